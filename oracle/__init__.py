@@ -1,0 +1,175 @@
+"""Python handle on the CPU oracle (oracle/kvo.c).  TEST INFRASTRUCTURE ONLY.
+
+Only tests, the package smoke check and the benchmark's CPU-baseline leg may
+import this module.  It compiles kvo.c with gcc (OpenMP, no fast-math, no FMA
+contraction) into oracle/libkvo.so and calls it through ctypes.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+import time
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "kvo.c")
+_LIB = os.path.join(_HERE, "libkvo.so")
+
+KVO_F32, KVO_BF16, KVO_F64 = 0, 1, 2
+_NP = {KVO_F32: np.float32, KVO_BF16: np.uint16, KVO_F64: np.float64}
+
+
+def build(src: str = _SRC, out: str = _LIB, extra_flags: Sequence[str] = ()) -> str:
+    """Compile the oracle (also used by mutation tests on patched copies)."""
+    cmd = ["gcc", "-O2", "-std=gnu11", "-fopenmp", "-fPIC", "-shared", "-ffp-contract=off",
+           "-fno-fast-math", "-I", _HERE, *extra_flags, src, "-o", out + ".tmp", "-lm"]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    os.replace(out + ".tmp", out)
+    return out
+
+
+class _Model(C.Structure):
+    _fields_ = [("num_layers", C.c_int32), ("hidden", C.c_int32), ("num_q_heads", C.c_int32),
+                ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn_dim", C.c_int32),
+                ("vocab", C.c_int32), ("rms_eps", C.c_double), ("rope_theta", C.c_double),
+                ("dtype", C.c_int32)]
+
+
+class _Layer(C.Structure):
+    _fields_ = [(k, C.c_void_p) for k in ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm",
+                                          "w_gate", "w_up", "w_down")]
+
+
+class _Arena(C.Structure):
+    _fields_ = [("base", C.c_void_p), ("block_size", C.c_int32), ("num_blocks", C.c_int64)]
+
+
+class Oracle:
+    """ctypes wrapper around one compiled copy of the oracle."""
+
+    def __init__(self, lib_path: Optional[str] = None):
+        path = lib_path or _LIB
+        if lib_path is None and (not os.path.exists(path)
+                                 or os.path.getmtime(path) < os.path.getmtime(_SRC)):
+            build()
+        self.lib = C.CDLL(path)
+        I32P = C.POINTER(C.c_int32)
+        for name in ("kvo_rebuild", "kvo_decode"):
+            f = getattr(self.lib, name)
+            f.restype = C.c_int
+            f.argtypes = [C.POINTER(_Model), C.c_void_p, C.POINTER(_Layer), I32P, I32P, C.c_int32,
+                          I32P, C.c_int32, C.POINTER(_Arena), C.c_void_p]
+        self.lib.kvo_layer0_kv.restype = C.c_int
+        self.lib.kvo_layer0_kv.argtypes = [C.POINTER(_Model), C.c_void_p, C.POINTER(_Layer),
+                                           I32P, I32P, C.c_int64, C.c_void_p, C.c_void_p]
+        self.lib.kvo_time_layers.restype = C.c_int
+        self.lib.kvo_time_layers.argtypes = [C.POINTER(_Model), C.c_void_p, C.POINTER(_Layer),
+                                             I32P, C.c_int32, C.c_int32]
+        self.lib.kvo_round_bf16.restype = C.c_uint16
+        self.lib.kvo_round_bf16.argtypes = [C.c_float]
+        self.lib.kvo_num_threads.restype = C.c_int
+
+    # -- marshalling -------------------------------------------------
+    @staticmethod
+    def _model(shape, dtype: Optional[int] = None, num_layers: Optional[int] = None) -> _Model:
+        return _Model(num_layers if num_layers is not None else shape.num_layers, shape.hidden,
+                      shape.num_q_heads, shape.num_kv_heads, shape.head_dim, shape.ffn_dim,
+                      shape.vocab, float(shape.rms_eps), float(shape.rope_theta),
+                      shape.dtype if dtype is None else dtype)
+
+    @staticmethod
+    def _check(a: np.ndarray, dt: int) -> np.ndarray:
+        assert a.dtype == _NP[dt] and a.flags.c_contiguous, (a.dtype, dt)
+        return a
+
+    def _layers(self, weights: Dict, dt: int):
+        arr = (_Layer * len(weights["layers"]))()
+        for i, lw in enumerate(weights["layers"]):
+            for k in _Layer._fields_:
+                setattr(arr[i], k[0], self._check(lw[k[0]], dt).ctypes.data)
+        return arr
+
+    @staticmethod
+    def _i32(a) -> np.ndarray:
+        return np.ascontiguousarray(a, dtype=np.int32)
+
+    # -- calls --------------------------------------------------------
+    def rebuild(self, shape, weights: Dict, tokens, lens, tables, arena: np.ndarray,
+                block_size: int, num_blocks: int, mode: str = "prefill",
+                dtype: Optional[int] = None, final_hidden: bool = False):
+        """Run the oracle in place on `arena` (raw host array of the dtype).
+        Returns the final fp64 hidden state [T, H] when final_hidden is set."""
+        dt = shape.dtype if dtype is None else dtype
+        m = self._model(shape, dt)
+        tokens, lens = self._i32(tokens), self._i32(lens)
+        tables = self._i32(tables)
+        max_blocks = tables.shape[1] if tables.ndim == 2 else 0
+        layers = self._layers(weights, dt)
+        emb = self._check(weights["embed"], dt)
+        need = shape.num_layers * 2 * num_blocks * block_size * shape.num_kv_heads * shape.head_dim
+        assert arena.dtype == _NP[dt] or (dt != KVO_F64 and arena.itemsize == np.dtype(_NP[dt]).itemsize)
+        assert arena.flags.c_contiguous and arena.size >= need, "arena smaller than its geometry"
+        assert tokens.shape[0] == int(lens.sum())
+        assert tables.ndim == 2 and tables.shape[0] == len(lens)
+        ar = _Arena(arena.ctypes.data, block_size, num_blocks)
+        fh = np.zeros((int(lens.sum()), shape.hidden), np.float64) if final_hidden else None
+        fn = self.lib.kvo_rebuild if mode == "prefill" else self.lib.kvo_decode
+        I32P = C.POINTER(C.c_int32)
+        rc = fn(C.byref(m), emb.ctypes.data, layers, tokens.ctypes.data_as(I32P),
+                lens.ctypes.data_as(I32P), len(lens), tables.ctypes.data_as(I32P), max_blocks,
+                C.byref(ar), fh.ctypes.data if fh is not None else None)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        return fh
+
+    def layer0_kv(self, shape, embed: np.ndarray, layer0: Dict, tokens, positions,
+                  dtype: Optional[int] = None):
+        dt = shape.dtype if dtype is None else dtype
+        m = self._model(shape, dt)
+        tokens, positions = self._i32(tokens), self._i32(positions)
+        n = tokens.shape[0]
+        kvd = shape.num_kv_heads * shape.head_dim
+        k = np.zeros((n, kvd), _NP[dt])
+        v = np.zeros((n, kvd), _NP[dt])
+        lay = self._layers({"layers": [layer0]}, dt)
+        I32P = C.POINTER(C.c_int32)
+        rc = self.lib.kvo_layer0_kv(C.byref(m), self._check(embed, dt).ctypes.data, lay,
+                                    tokens.ctypes.data_as(I32P), positions.ctypes.data_as(I32P),
+                                    n, k.ctypes.data, v.ctypes.data)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        return k, v
+
+    def time_layers(self, shape, weights: Dict, tokens, num_layers: int) -> float:
+        """Wall time of `num_layers` full layers over one request of len(tokens)."""
+        dt = shape.dtype
+        m = self._model(shape, dt)
+        tokens = self._i32(tokens)
+        lay = self._layers(weights, dt)
+        I32P = C.POINTER(C.c_int32)
+        t0 = time.perf_counter()
+        rc = self.lib.kvo_time_layers(C.byref(m), self._check(weights["embed"], dt).ctypes.data,
+                                      lay, tokens.ctypes.data_as(I32P), tokens.shape[0], num_layers)
+        t1 = time.perf_counter()
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        return t1 - t0
+
+    def round_bf16(self, x: float) -> int:
+        return int(self.lib.kvo_round_bf16(float(x)))
+
+    def num_threads(self) -> int:
+        return int(self.lib.kvo_num_threads())
+
+
+_default: Optional[Oracle] = None
+
+
+def get() -> Oracle:
+    global _default
+    if _default is None:
+        _default = Oracle()
+    return _default

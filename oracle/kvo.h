@@ -1,0 +1,94 @@
+/*
+ * kvo.h -- CPU oracle for the KV rebuild.  TEST INFRASTRUCTURE ONLY.
+ *
+ * This is the plain, slow reference that the HIP rebuild is checked against.
+ * Only the test suite, the package smoke check and the benchmark's CPU
+ * baseline may load it; the product library never calls into it, and the two
+ * share no code, headers or tables.
+ *
+ * What it computes: the re-prefill that rebuilds request-specific KV contents
+ * from logged token prefixes into a retained raw KV arena after a worker
+ * failure (Sec. 4.2 Handover, step 5; Sec. 4.3 LLM Context Recovery), with the
+ * whole pool flushed and refilled because complete KV contents are not
+ * trusted across the failure (Sec. 4.2, flush-and-refill paragraph; Sec. 2.3
+ * Finding 2).  The paper does not write out the model forward; the oracle
+ * takes a Llama-style pre-norm decoder (RMSNorm, Q/K/V projections, NeoX
+ * half-split RoPE, causal GQA softmax attention, output projection, SwiGLU
+ * FFN, fp32 residual stream) and writes the rotated K and the V of every
+ * position of every layer into a paged arena through per-request block tables.
+ *
+ * Precision contract: every reduction is accumulated in fp64; every op output
+ * is rounded to fp32 (the working precision) and, for bf16 models, the
+ * normed activations, rotated Q/K, V, the attention output and the SwiGLU
+ * output are rounded to bf16 (round-to-nearest-even).  dtype KVO_F64 is a pin
+ * mode in which nothing is rounded at all.
+ */
+#ifndef KVO_ORACLE_H
+#define KVO_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { KVO_F32 = 0, KVO_BF16 = 1, KVO_F64 = 2 };
+
+typedef struct {
+  int32_t num_layers, hidden, num_q_heads, num_kv_heads, head_dim, ffn_dim, vocab;
+  double rms_eps, rope_theta;
+  int32_t dtype;         /* element type of weights and arena: KVO_F32/BF16/F64 */
+} kvo_model;
+
+/* One layer's weights, host pointers, nn.Linear layout [out, in] row-major. */
+typedef struct {
+  const void *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *w_gate, *w_up, *w_down;
+} kvo_layer;
+
+/* Paged arena (host memory): element offset of (layer l, plane kv, block b,
+ * slot s, kv head h, dim e) is ((((l*2+kv)*num_blocks+b)*block_size+s)*nkv+h)*d+e. */
+typedef struct {
+  void* base;
+  int32_t block_size;
+  int64_t num_blocks;
+} kvo_arena;
+
+/* Prefill mode: all positions of each request per layer.
+ * tokens: packed [sum(lens)]; block_tables: [R][max_blocks].
+ * final_hidden (optional, may be NULL): [sum(lens)][hidden] fp64 residual
+ * after the last layer's FFN (computed only when non-NULL).
+ * Returns 0 on success, -1 on an invalid argument. */
+int kvo_rebuild(const kvo_model* m, const void* embed, const kvo_layer* layers,
+                const int32_t* tokens, const int32_t* lens, int32_t num_requests,
+                const int32_t* block_tables, int32_t max_blocks,
+                kvo_arena* arena, double* final_hidden);
+
+/* Decode mode: the same requests fed one token at a time through all layers,
+ * attention reading past K/V back from the arena through the block table. */
+int kvo_decode(const kvo_model* m, const void* embed, const kvo_layer* layers,
+               const int32_t* tokens, const int32_t* lens, int32_t num_requests,
+               const int32_t* block_tables, int32_t max_blocks,
+               kvo_arena* arena, double* final_hidden);
+
+/* Layer-0 rounded K and V rows (each num_kv_heads*head_dim elements of the
+ * model dtype, written to k_out / v_out) for (token, position) pairs; layer 0
+ * depends on nothing else, so sampled positions of a large batch can be
+ * checked one by one. */
+int kvo_layer0_kv(const kvo_model* m, const void* embed, const kvo_layer* layer0,
+                  const int32_t* tokens, const int32_t* positions, int64_t n,
+                  void* k_out, void* v_out);
+
+/* Run layers [0, num_layers) of one request of n tokens without an arena
+ * (scratch K/V), used to time the oracle on a bounded sample. */
+int kvo_time_layers(const kvo_model* m, const void* embed, const kvo_layer* layers,
+                    const int32_t* tokens, int32_t n, int32_t num_layers);
+
+/* fp32 -> bf16 bits exactly as the oracle rounds (exported for its pins). */
+uint16_t kvo_round_bf16(float x);
+
+/* OpenMP threads the oracle runs with. */
+int kvo_num_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,76 @@
+"""Mutation check of the oracle's pins: each plausible mistake planted in a
+copy of the oracle source (on the CPU) must make at least one pin fail."""
+import os
+import re
+import shutil
+import subprocess
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+import pytest
+
+import oracle
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(os.path.dirname(HERE), "oracle", "kvo.c")
+
+# (name, exact text in kvo.c, replacement, which occurrence (0-based))
+MUTANTS = [
+    ("rope_sign", "hu[i] = to_work(a * c - b * s, dt);", "hu[i] = to_work(a * c + b * s, dt);", 0),
+    ("rope_frequency", "pow(theta, -(double)(2 * i) / (double)d)", "pow(theta, -(double)(i) / (double)d)", 0),
+    ("rope_pairing", "double a = hu[i], b = hu[i + half];", "double a = hu[2 * (i / 2)], b = hu[2 * (i / 2) + 1];", 0),
+    ("dropped_norm_gain", "rnd(load(g, dt, j) * xr[j] * inv, dt)", "rnd(xr[j] * inv, dt)", 0),
+    ("norm_sum_not_mean", "inv = 1.0 / sqrt(ss / (double)H + eps);", "inv = 1.0 / sqrt(ss + eps);", 0),
+    ("gqa_modulo_grouping", "kvh = h / g,", "kvh = h % nkv,", 0),
+    ("no_softmax_scale", "z[j] = s * scale;", "z[j] = s;", 0),
+    ("no_softmax_denominator", "rnd(to_work(o / den, dt), dt)", "rnd(to_work(o, dt), dt)", 0),
+    ("v_from_k_plane", "arena_off(m, ar, l, 1, slot_of(ar, table, j))", "arena_off(m, ar, l, 0, slot_of(ar, table, j))", 0),
+    ("no_attention_residual", "x[idx] = to_work(x[idx] + a[idx], dt);", "x[idx] = to_work(a[idx], dt);", 0),
+    ("no_ffn_residual", "x[idx] = to_work(x[idx] + a[idx], dt);", "x[idx] = to_work(a[idx], dt);", 1),
+    ("sigmoid_not_silu", "gv / (1.0 + exp(-gv))", "1.0 / (1.0 + exp(-gv))", 0),
+    ("dropped_up_projection", "rnd(to_work(silu * up[idx], dt), dt)", "rnd(to_work(silu, dt), dt)", 0),
+    ("slot_offset", "table[p / ar->block_size] * ar->block_size + p % ar->block_size",
+     "table[p / ar->block_size] * ar->block_size + (p + 1) % ar->block_size", 0),
+    ("bf16_truncation", "u += 0x7fffu + ((u >> 16) & 1u);", "u += 0u;", 0),
+    ("gate_up_swapped", "project(lw->w_gate, dt, F, H, a, cnt, gate);", "project(lw->w_up, dt, F, H, a, cnt, gate);", 0),
+    ("k_not_rotated", "rope_row(k + r * nkv * d, (int)nkv, (int)d, p, m->rope_theta, dt);", ";", 0),
+    ("position_plus_one", "double phi = (double)pos * inv_freq;", "double phi = (double)(pos + 1) * inv_freq;", 0),
+    ("no_rounding_of_q", "q[r * nq * d + e] = rnd(q[r * nq * d + e], dt);", "q[r * nq * d + e] = q[r * nq * d + e];", 0),
+]
+
+
+def _patch(text, old, new, occ):
+    idx = -1
+    for _ in range(occ + 1):
+        idx = text.find(old, idx + 1)
+        assert idx >= 0, f"anchor not found: {old}"
+    return text[:idx] + new + text[idx + len(old):]
+
+
+def _run_mutant(tmp, name, old, new, occ):
+    d = os.path.join(tmp, name)
+    os.makedirs(d, exist_ok=True)
+    src = open(SRC).read()
+    shutil.copy(os.path.join(os.path.dirname(SRC), "kvo.h"), d)
+    with open(os.path.join(d, "kvo.c"), "w") as f:
+        f.write(_patch(src, old, new, occ))
+    lib = oracle.build(os.path.join(d, "kvo.c"), os.path.join(d, "libkvo.so"), ["-I", d])
+    env = dict(os.environ, OMP_NUM_THREADS="2")
+    p = subprocess.run([sys.executable, os.path.join(HERE, "oracle_pins.py"), lib],
+                       capture_output=True, text=True, timeout=600, env=env)
+    m = re.search(r"(\d+) of (\d+) pins failed", p.stdout)
+    caught = (int(m.group(1)) if m else 1) if p.returncode == 0 or m is None else int(m.group(1))
+    return name, caught, p.stdout[-2000:] + p.stderr[-500:]
+
+
+def test_every_anchor_exists():
+    src = open(SRC).read()
+    for name, old, new, occ in MUTANTS:
+        _patch(src, old, new, occ)
+
+
+def test_mutants_are_caught(tmp_path):
+    with ThreadPoolExecutor(max_workers=4) as ex:
+        results = list(ex.map(lambda m: _run_mutant(str(tmp_path), *m), MUTANTS))
+    missed = [(n, out) for n, caught, out in results if caught == 0]
+    assert not missed, "mutants not caught by any pin: " + ", ".join(n for n, _ in missed)
