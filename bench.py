@@ -1,0 +1,233 @@
+"""KV-rebuild benchmark on one MI355X.
+
+    python bench.py [--gpus 1] [--steps 5] [--warmup 1] [--config 2]
+
+A step is one full rebuild (kv_rebuild_execute of a staged plan: embedding
+gather, every layer's norms, QKV GEMM + RoPE + arena scatter, attention,
+output projection, SwiGLU FFN) of the configuration's whole request batch,
+with weights, arena and the staged metadata already resident in HBM.  The
+default workload is the 8B-shaped decoder with 16 requests of 2048-16384
+tokens.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import subprocess
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2517.0   # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 flop/clk)
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def algorithmic_work(wl):
+    """Flops and HBM bytes the method must spend (last layer: K/V projections only)."""
+    s = wl.shape
+    H, d, nq, nkv, F, L = s.hidden, s.head_dim, s.num_q_heads, s.num_kv_heads, s.ffn_dim, s.num_layers
+    lin_tok = 2.0 * ((L - 1) * (H * (nq + 2 * nkv) * d + nq * d * H + 3 * H * F) + 2 * H * nkv * d)
+    n = wl.lens.astype(np.float64)
+    attn = float(np.sum(2.0 * nq * d * n * (n + 1))) * (L - 1)
+    flops = lin_tok * wl.total_tokens + attn
+    e = s.elem_bytes
+    w_layer = H * (nq + 2 * nkv) * d + nq * d * H + 3 * H * F + 2 * H
+    weights = ((L - 1) * w_layer + 2 * nkv * d * H + H) * e
+    kv = wl.total_tokens * L * 2 * nkv * d * e
+    emb = wl.total_tokens * H * e
+    return {"flops": flops, "linear_flops": lin_tok * wl.total_tokens, "attn_flops": attn,
+            "bytes": float(weights + kv + emb), "kv_bytes": float(kv)}
+
+
+def cpu_model(name: str) -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor()
+
+
+def cpu_baseline(wl, model, Hn):
+    """Time the CPU oracle on a bounded sample of the same workload and model
+    the full rebuild from it: one layer at two request lengths gives
+    t_layer(n) = a n + b n^2, layer-0 K/V rows give the last-layer cost per
+    token; t = sum_r (L-1) t_layer(n_r) + c n_r."""
+    import oracle
+    o = oracle.get()
+    s = wl.shape
+    host = Hn.host_copy_layer0(model)
+    layer_w = {"embed": host["embed"], "layers": [host["layer0"]]}
+    rng = np.random.default_rng(99)
+    per_tok_gflop = 2 * (s.hidden * (s.num_q_heads + 2 * s.num_kv_heads) * s.head_dim
+                         + s.num_q_heads * s.head_dim * s.hidden + 3 * s.hidden * s.ffn_dim) / 1e9
+    # sample sizes chosen for ~10-30 s of oracle work on a 16-thread host (~20 GFLOP/s fp64)
+    n1 = int(min(512, max(64, (80.0 / per_tok_gflop) // 16 * 16)))
+    n2 = 3 * n1
+    if s.num_layers == 2 and s.hidden <= 512:  # tiny configuration: run it whole
+        n1, n2 = int(wl.lens.min()), int(wl.lens.max())
+    t1 = o.time_layers(s, layer_w, rng.integers(0, s.vocab, n1), 1)
+    t2 = o.time_layers(s, layer_w, rng.integers(0, s.vocab, n2), 1)
+    b = max(0.0, (t2 / n2 - t1 / n1) / (n2 - n1))
+    a = max(1e-12, t1 / n1 - b * n1)
+    nk = 128
+    tk0 = time.perf_counter()
+    o.layer0_kv(s, host["embed"], host["layer0"], rng.integers(0, s.vocab, nk),
+                rng.integers(0, 4096, nk))
+    c = (time.perf_counter() - tk0) / nk
+    n = wl.lens.astype(np.float64)
+    t_pred = float(np.sum((s.num_layers - 1) * (a * n + b * n * n) + c * n))
+    return {"value": wl.total_tokens / t_pred, "unit": "tokens/s", "cores": o.num_threads(),
+            "kind": "oracle",
+            "sample": (f"oracle timed on one layer of the same shape at n={n1} ({t1:.1f}s) and "
+                       f"n={n2} ({t2:.1f}s) plus layer-0 K/V rows of {nk} tokens ({c * nk:.2f}s); "
+                       f"fitted t_layer(n)=a*n+b*n^2 extrapolated to {s.num_layers} layers x "
+                       f"{wl.num_requests} requests (modelled, {t_pred:.0f}s predicted)"),
+            "host_cpu": cpu_model("")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--wave-tokens", type=int, default=0, help="0 = largest that fits")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-check", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+    from paper_2608_14635_amd import harness as Hn
+    from paper_2608_14635_amd import kvr
+    from paper_2608_14635_amd import workloads as W
+
+    torch.cuda.set_device(0)
+    cfg = args.config
+    shape = {1: W.TINY_F32, 2: W.LLAMA8B, 3: W.LLAMA8B, 4: W.QWEN14B, 5: W.QWEN32B}[cfg]
+    log = lambda m: print(m, file=sys.stderr, flush=True)  # noqa: E731
+
+    log(f"[bench] config {cfg}: generating weights on the device")
+    model = Hn.device_model_random(shape, seed=0x5EED0000 + cfg)
+    torch.cuda.synchronize()
+    if cfg in (3, 5):
+        # arena fills the HBM left after weights and workspace (2 GiB margin)
+        probe = W.CONFIGS[cfg](num_blocks=1 << 30)
+        wave = args.wave_tokens or min(probe.total_tokens, 131072)
+        ws_bytes = kvr.kv_rebuild_workspace_bytes(shape, probe.num_requests, probe.total_tokens, wave)
+        free, _ = torch.cuda.mem_get_info()
+        per_block = shape.num_layers * 2 * 16 * shape.kv_row_elems() * shape.elem_bytes
+        nb = int((free - ws_bytes - (2 << 30)) // per_block)
+        wl = W.CONFIGS[cfg](num_blocks=nb)
+    else:
+        wl = W.CONFIGS[cfg]()
+    T = wl.total_tokens
+    wave = args.wave_tokens or min(T, 131072 if cfg != 5 else 65536)
+    log(f"[bench] R={wl.num_requests} T={T} NB={wl.num_blocks} arena={wl.arena_bytes() / 2**30:.1f} GiB")
+    arena = Hn.DeviceArena(wl)
+    arena.bind(0)
+    ws, nbytes = Hn.alloc_workspace(shape, wl.num_requests, T, wave)
+    stream = Hn.stream_ptr()
+    plan = kvr.kv_rebuild_stage(arena.handle, wl.tokens, wl.lens, wl.block_tables, ws.data_ptr(),
+                                nbytes, stream)
+    n_waves, max_wave = kvr.kv_plan_info(plan)
+    torch.cuda.synchronize()
+
+    for i in range(args.warmup):
+        kvr.kv_rebuild_execute(model.weights, plan, stream)
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for i in range(args.steps):
+        kvr.kv_rebuild_execute(model.weights, plan, stream)
+    ev1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_wall = (t1 - t0) * 1e3 / args.steps
+    ms_ev = ev0.elapsed_time(ev1) / args.steps
+    log(f"[bench] {args.steps} steps: {ms_wall:.1f} ms/step wall, {ms_ev:.1f} ms/step events")
+
+    # one profiled step: per-kernel-class device time via HIP events inside the library
+    kvr.kv_profile_reset(arena.handle)
+    kvr.kv_profile_enable(arena.handle, True)
+    kvr.kv_rebuild_execute(model.weights, plan, stream)
+    torch.cuda.synchronize()
+    prof = kvr.kv_profile_read(arena.handle)
+    kvr.kv_profile_enable(arena.handle, False)
+    kvr.kv_plan_release(plan)
+
+    # PCIe-inclusive rate (host arrays staged every call), for reference only
+    torch.cuda.synchronize()
+    tp0 = time.perf_counter()
+    kvr.kv_rebuild(model.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle, ws.data_ptr(),
+                   nbytes, stream)
+    torch.cuda.synchronize()
+    ms_pcie = (time.perf_counter() - tp0) * 1e3
+
+    check = None
+    if not args.no_check:
+        check = arena.check_invariants()
+        log(f"[bench] arena invariants after the last rebuild: {check}")
+
+    work = algorithmic_work(wl)
+    peak = PEAK_FP32_TFLOPS if shape.dtype == W.F32 else PEAK_BF16_TFLOPS
+    sec = ms_wall / 1e3
+    dom = max((k for k in prof if prof[k]["launches"]), key=lambda k: prof[k]["ms"])
+    dom_t = prof[dom]["ms"] / 1e3
+    dom_tf = prof[dom]["flops"] / dom_t / 1e12 if dom_t > 0 else 0.0
+    gemm_keys = ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down")
+    gemm_ms = sum(prof[k]["ms"] for k in gemm_keys)
+    gemm_tf = sum(prof[k]["flops"] for k in gemm_keys) / (gemm_ms / 1e3) / 1e12 if gemm_ms else 0.0
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(wl, model, Hn)
+        log(f"[bench] cpu baseline {cpu}")
+
+    dt_name = "bf16" if shape.dtype == W.BF16 else "f32"
+    out = {
+        "metric": "KV-rebuild prefix tokens/sec (1 GPU) + MFMA/HBM roofline fraction",
+        "value": T / sec, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_wall, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": dt_name, "data": "synthetic",
+        "config": {"workload": wl.name, "requests": wl.num_requests, "total_tokens": T,
+                   "block_size": wl.block_size, "num_blocks": wl.num_blocks,
+                   "layers": shape.num_layers, "hidden": shape.hidden,
+                   "heads": f"{shape.num_q_heads}/{shape.num_kv_heads}x{shape.head_dim}",
+                   "ffn": shape.ffn_dim, "vocab": shape.vocab, "waves": n_waves,
+                   "max_wave_tokens": max_wave, "weights": "random N(0,0.02)"},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": dom_tf, "peak": peak,
+                     "unit": "TFLOP/s", "frac": dom_tf / peak, "traffic": None},
+        "end_to_end": {"algorithmic_tflop": work["flops"] / 1e12,
+                       "mfma_frac": work["flops"] / sec / 1e12 / peak,
+                       "hbm_frac": work["bytes"] / sec / 1e9 / PEAK_HBM_GBS,
+                       "gemm_tflops": gemm_tf, "gemm_frac": gemm_tf / peak,
+                       "ms_per_step_events": ms_ev, "pcie_inclusive_ms": ms_pcie},
+        "kernel_classes": {k: {"ms": round(v["ms"], 3), "launches": v["launches"],
+                               "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["ms"] and v["flops"] else None}
+                           for k, v in prof.items()},
+        "arena_check": check,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    arena.release()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,760 @@
+// C ABI of the KV-rebuild library: argument validation, wave planning,
+// metadata staging and the per-layer kernel sequence.  Host code only; the
+// kernels live in misc.hip, gemm_bf16.hip, gemm_f32.hip and attention.hip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "kvr.h"
+#include "kvr_profile.h"
+#include "launch.h"
+
+using namespace kvr;
+
+namespace {
+
+thread_local std::string g_err;
+
+kv_status fail(kv_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+kv_status ok() {
+  g_err.clear();
+  return KV_OK;
+}
+
+int64_t elem_bytes(int32_t dtype) { return dtype == KV_BF16 ? 2 : 4; }
+int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+kv_status check_desc(const kv_model_desc* d) {
+  if (!d) return fail(KV_EINVAL, "null model description");
+  if (d->num_layers <= 0 || d->hidden <= 0 || d->num_q_heads <= 0 || d->num_kv_heads <= 0 ||
+      d->head_dim <= 0 || d->ffn_dim <= 0 || d->vocab <= 0)
+    return fail(KV_EINVAL, "model dimensions must be positive");
+  if (!(d->rms_eps >= 0.0) || !(d->rope_theta > 0.0))
+    return fail(KV_EINVAL, "rms_eps must be >= 0 and rope_theta > 0");
+  if (d->num_q_heads % d->num_kv_heads != 0)
+    return fail(KV_EINVAL, "num_q_heads must be a multiple of num_kv_heads");
+  if (d->hidden % 8 != 0 || d->hidden > 8192)
+    return fail(KV_EINVAL, "hidden must be a multiple of 8 and at most 8192");
+  if (d->dtype == KV_BF16) {
+    if (d->head_dim != 128) return fail(KV_EINVAL, "bf16 models need head_dim == 128");
+    if (d->hidden % 256 != 0) return fail(KV_EINVAL, "bf16 models need hidden % 256 == 0");
+    if (d->num_kv_heads % 2 != 0) return fail(KV_EINVAL, "bf16 models need an even num_kv_heads");
+    if (d->ffn_dim % 128 != 0) return fail(KV_EINVAL, "bf16 models need ffn_dim % 128 == 0");
+  } else if (d->dtype == KV_F32) {
+    if (d->head_dim % 2 != 0 || 128 % d->head_dim != 0 || d->head_dim < 16)
+      return fail(KV_EINVAL, "fp32 models need head_dim in {16, 32, 64, 128}");
+    if ((d->num_kv_heads * d->head_dim) % 128 != 0 || (d->num_q_heads * d->head_dim) % 128 != 0)
+      return fail(KV_EINVAL, "fp32 models need nq*d and nkv*d multiples of 128");
+    if (d->hidden % 128 != 0) return fail(KV_EINVAL, "fp32 models need hidden % 128 == 0");
+    if (d->ffn_dim % 8 != 0) return fail(KV_EINVAL, "fp32 models need ffn_dim % 8 == 0");
+  } else {
+    return fail(KV_EINVAL, "unknown dtype %d", d->dtype);
+  }
+  return KV_OK;
+}
+
+bool same_desc(const kv_model_desc& a, const kv_model_desc& b) {
+  return a.num_layers == b.num_layers && a.hidden == b.hidden && a.num_q_heads == b.num_q_heads &&
+         a.num_kv_heads == b.num_kv_heads && a.head_dim == b.head_dim && a.ffn_dim == b.ffn_dim &&
+         a.vocab == b.vocab && a.rms_eps == b.rms_eps && a.rope_theta == b.rope_theta &&
+         a.dtype == b.dtype;
+}
+
+// ---------------------------------------------------------------------------
+// Workspace layout (256-byte aligned segments; metadata first so that one
+// host->device copy stages it)
+// ---------------------------------------------------------------------------
+struct Layout {
+  int64_t T = 0, W = 0, Wpad = 0, nqblk_cap = 0;
+  size_t tok = 0, pos = 0, slot = 0, qblk = 0, meta_end = 0;
+  size_t rope = 0, x = 0, a = 0, q = 0, u = 0, vt = 0, hf = 0, total = 0;
+};
+
+Layout make_layout(const kv_model_desc& d, int32_t R, int64_t T, int64_t W) {
+  Layout L;
+  L.T = T;
+  L.W = W;
+  L.Wpad = round_up(std::max<int64_t>(W, 1), 256);
+  L.nqblk_cap = (T + ATTN_QBLOCK - 1) / ATTN_QBLOCK + R;
+  const int64_t e = elem_bytes(d.dtype);
+  size_t off = 0;
+  auto seg = [&](size_t bytes) {
+    const size_t at = off;
+    off = (size_t)round_up((int64_t)(off + bytes), 256);
+    return at;
+  };
+  L.tok = seg(4 * (size_t)T);
+  L.pos = seg(4 * (size_t)T);
+  L.slot = seg(8 * (size_t)T);
+  L.qblk = seg(16 * (size_t)L.nqblk_cap);
+  L.meta_end = off;
+  L.rope = seg((size_t)8 * L.Wpad * (d.head_dim / 2));
+  L.x = seg((size_t)4 * L.Wpad * d.hidden);
+  L.a = seg((size_t)e * L.Wpad * d.hidden);
+  L.q = seg((size_t)e * L.Wpad * d.num_q_heads * d.head_dim);
+  L.u = seg((size_t)e * L.Wpad * d.num_q_heads * d.head_dim);
+  L.vt = seg(d.dtype == KV_BF16 ? (size_t)2 * d.num_kv_heads * d.head_dim * L.Wpad : 0);
+  L.hf = seg((size_t)e * L.Wpad * d.ffn_dim);
+  L.total = off;
+  return L;
+}
+
+// ---------------------------------------------------------------------------
+// Handles
+// ---------------------------------------------------------------------------
+struct Wave {
+  int64_t tok_begin;
+  int32_t rows;
+  int32_t qblk_begin, num_qblk;
+  double causal_pairs;  // sum over its requests of n(n+1)/2 (query, key) pairs
+};
+
+}  // namespace
+
+struct kv_arena {
+  void* base;
+  uint64_t bytes;
+  kv_model_desc desc;
+  int32_t block_size;
+  int64_t num_blocks;
+  int32_t device;
+  int* probe_flag;
+  // pinned host staging for metadata uploads; reused after its last copy completed
+  void* pinned = nullptr;
+  size_t pinned_bytes = 0;
+  hipEvent_t staged = nullptr;
+  bool staged_pending = false;
+  // optional per-kernel-class timing
+  bool profile = false;
+  std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> prof_pending;
+  std::vector<hipEvent_t> prof_pool;
+  double prof_ms[KV_PROF_CLASSES] = {};
+  int64_t prof_launches[KV_PROF_CLASSES] = {};
+  double prof_flops[KV_PROF_CLASSES] = {};
+  std::vector<double> pending_flops;
+};
+
+struct kv_plan {
+  kv_arena* arena;
+  char* ws;
+  uint64_t ws_bytes;
+  Layout lay;
+  std::vector<Wave> waves;
+  int32_t max_len;
+};
+
+namespace {
+
+std::mutex g_reg_mu;
+std::set<const void*> g_arenas, g_plans;
+
+bool live_arena(const kv_arena* a) {
+  std::lock_guard<std::mutex> g(g_reg_mu);
+  return a && g_arenas.count(a);
+}
+bool live_plan(const kv_plan* p) {
+  std::lock_guard<std::mutex> g(g_reg_mu);
+  return p && g_plans.count(p);
+}
+
+struct DeviceGuard {
+  int prev = -1;
+  bool changed = false;
+  hipError_t err = hipSuccess;
+  explicit DeviceGuard(int dev) {
+    err = hipGetDevice(&prev);
+    if (err == hipSuccess && prev != dev) {
+      err = hipSetDevice(dev);
+      changed = err == hipSuccess;
+    }
+  }
+  ~DeviceGuard() {
+    if (changed) (void)hipSetDevice(prev);
+  }
+};
+
+kv_status check_request(const kv_model_desc* desc, int32_t B, int64_t NB, const int32_t* tokens,
+                        const int32_t* lens, int32_t R, const int32_t* tables, int32_t max_blocks,
+                        int64_t* total_out, int32_t* max_len_out) {
+  kv_status st = check_desc(desc);
+  if (st != KV_OK) return st;
+  if (B <= 0 || NB <= 0) return fail(KV_EINVAL, "block_size and num_blocks must be positive");
+  if (R < 0) return fail(KV_EINVAL, "num_requests < 0");
+  if (max_blocks < 0) return fail(KV_EINVAL, "max_blocks_per_req < 0");
+  if (R > 0 && !lens) return fail(KV_EINVAL, "null prefix_lens");
+  int64_t T = 0;
+  int32_t max_len = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    if (lens[r] < 0) return fail(KV_EINVAL, "prefix_lens[%d] = %d < 0", r, lens[r]);
+    T += lens[r];
+    max_len = std::max(max_len, lens[r]);
+  }
+  if (T > (int64_t)INT32_MAX) return fail(KV_EINVAL, "more than 2^31-1 prefix tokens in one call");
+  if (T > 0 && !tokens) return fail(KV_EINVAL, "null token_prefixes");
+  if (T > 0 && !tables) return fail(KV_EINVAL, "null block_tables");
+  for (int32_t r = 0; r < R; ++r) {
+    const int64_t nb = ((int64_t)lens[r] + B - 1) / B;
+    if (nb > max_blocks)
+      return fail(KV_ECAPACITY, "request %d needs %lld blocks > max_blocks_per_req %d", r,
+                  (long long)nb, max_blocks);
+  }
+  for (int64_t i = 0; i < T; ++i)
+    if (tokens[i] < 0 || tokens[i] >= desc->vocab)
+      return fail(KV_ERANGE, "token %d at index %lld outside [0, %d)", tokens[i], (long long)i,
+                  desc->vocab);
+  std::vector<uint8_t> seen((size_t)NB, 0);
+  for (int32_t r = 0; r < R; ++r) {
+    const int64_t nb = ((int64_t)lens[r] + B - 1) / B;
+    for (int64_t b = 0; b < nb; ++b) {
+      const int32_t blk = tables[(int64_t)r * max_blocks + b];
+      if (blk < 0 || blk >= NB)
+        return fail(KV_ERANGE, "block_tables[%d][%lld] = %d outside [0, %lld)", r, (long long)b,
+                    blk, (long long)NB);
+      if (seen[blk]) return fail(KV_EALIAS, "block %d listed twice", blk);
+      seen[blk] = 1;
+    }
+  }
+  if (total_out) *total_out = T;
+  if (max_len_out) *max_len_out = max_len;
+  return KV_OK;
+}
+
+// timing hooks around each launch when profiling is on
+struct ProfScope {
+  kv_arena* a;
+  hipStream_t s;
+  int cls;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  ProfScope(kv_arena* a_, hipStream_t s_, int cls_, double flops) : a(a_), s(s_), cls(cls_) {
+    if (!a->profile) return;
+    auto take = [&]() {
+      hipEvent_t e = nullptr;
+      if (!a->prof_pool.empty()) {
+        e = a->prof_pool.back();
+        a->prof_pool.pop_back();
+      } else {
+        (void)hipEventCreate(&e);
+      }
+      return e;
+    };
+    e0 = take();
+    e1 = take();
+    (void)hipEventRecord(e0, s);
+    a->pending_flops.push_back(flops);
+  }
+  ~ProfScope() {
+    if (!e0) return;
+    (void)hipEventRecord(e1, s);
+    a->prof_pending.push_back({cls, {e0, e1}});
+  }
+};
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Entry points
+// ---------------------------------------------------------------------------
+extern "C" {
+
+const char* kv_last_error(void) { return g_err.c_str(); }
+
+uint64_t kv_rebuild_workspace_bytes(const kv_model_desc* desc, int32_t num_requests,
+                                    int64_t total_tokens, int64_t wave_tokens) {
+  if (check_desc(desc) != KV_OK || num_requests < 0 || total_tokens < 0 || wave_tokens < 0)
+    return 0;
+  return make_layout(*desc, num_requests, total_tokens, std::min(wave_tokens, total_tokens)).total;
+}
+
+kv_status kv_rebuild_check(const kv_model_desc* desc, int32_t block_size, int64_t num_blocks,
+                           const int32_t* token_prefixes, const int32_t* prefix_lens,
+                           int32_t num_requests, const int32_t* block_tables,
+                           int32_t max_blocks_per_req) {
+  kv_status st = check_request(desc, block_size, num_blocks, token_prefixes, prefix_lens,
+                               num_requests, block_tables, max_blocks_per_req, nullptr, nullptr);
+  return st == KV_OK ? ok() : st;
+}
+
+kv_status kv_arena_bind(void* base, uint64_t bytes, const kv_model_desc* desc, int32_t block_size,
+                        int64_t num_blocks, int32_t device, kv_arena_t* out) {
+  if (!out) return fail(KV_EINVAL, "null output handle");
+  *out = nullptr;
+  if (!base) return fail(KV_EINVAL, "null arena base");
+  kv_status st = check_desc(desc);
+  if (st != KV_OK) return st;
+  if (block_size <= 0 || num_blocks <= 0)
+    return fail(KV_EINVAL, "block_size and num_blocks must be positive");
+  const unsigned __int128 need = (unsigned __int128)desc->num_layers * 2 * (uint64_t)num_blocks *
+                                 (uint64_t)block_size * desc->num_kv_heads * desc->head_dim *
+                                 elem_bytes(desc->dtype);
+  if (need > (unsigned __int128)bytes)
+    return fail(KV_EINVAL, "arena of %llu bytes is smaller than its geometry needs",
+                (unsigned long long)bytes);
+  const char* force = getenv("KVR_DEBUG_FAIL_PROBE");
+  if (force && force[0] == '1') return fail(KV_EDEVICE, "health probe failed (forced by KVR_DEBUG_FAIL_PROBE)");
+
+  DeviceGuard dg(device);
+  if (dg.err != hipSuccess) return fail(KV_EDEVICE, "cannot select device %d: %s", device, hipGetErrorString(dg.err));
+  hipPointerAttribute_t attr;
+  hipError_t e = hipPointerGetAttributes(&attr, base);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(KV_EDEVICE, "arena pointer not known to HIP: %s", hipGetErrorString(e));
+  }
+  if (attr.type != hipMemoryTypeDevice || attr.device != device)
+    return fail(KV_EDEVICE, "arena pointer is not device memory on device %d", device);
+  // health probe: a kernel round trip on the device (Sec. 4.2 step 2)
+  int* flag = nullptr;
+  if ((e = hipMalloc(&flag, sizeof(int))) != hipSuccess)
+    return fail(KV_EDEVICE, "probe allocation failed: %s", hipGetErrorString(e));
+  int host_flag = 0;
+  bool good = hipMemset(flag, 0, sizeof(int)) == hipSuccess && launch_probe(flag, nullptr) == 0 &&
+              hipMemcpy(&host_flag, flag, sizeof(int), hipMemcpyDeviceToHost) == hipSuccess &&
+              host_flag == 0x600D;
+  if (!good) {
+    (void)hipGetLastError();
+    (void)hipFree(flag);
+    return fail(KV_EDEVICE, "GPU health probe failed on device %d", device);
+  }
+  kv_arena* a = new (std::nothrow) kv_arena();
+  if (!a) {
+    (void)hipFree(flag);
+    return fail(KV_ENOMEM, "host allocation failed");
+  }
+  a->base = base;
+  a->bytes = bytes;
+  a->desc = *desc;
+  a->block_size = block_size;
+  a->num_blocks = num_blocks;
+  a->device = device;
+  a->probe_flag = flag;
+  if (hipEventCreateWithFlags(&a->staged, hipEventDisableTiming) != hipSuccess) {
+    (void)hipFree(flag);
+    delete a;
+    return fail(KV_EDEVICE, "event creation failed");
+  }
+  {
+    std::lock_guard<std::mutex> g(g_reg_mu);
+    g_arenas.insert(a);
+  }
+  *out = a;
+  return ok();
+}
+
+kv_status kv_arena_release(kv_arena_t a) {
+  {
+    std::lock_guard<std::mutex> g(g_reg_mu);
+    if (!a || !g_arenas.count(a)) return fail(KV_ESTATE, "unknown or released arena handle");
+    g_arenas.erase(a);
+  }
+  DeviceGuard dg(a->device);
+  if (a->staged_pending) (void)hipEventSynchronize(a->staged);
+  if (a->pinned) (void)hipHostFree(a->pinned);
+  (void)hipEventDestroy(a->staged);
+  for (auto& pe : a->prof_pending) {
+    (void)hipEventDestroy(pe.second.first);
+    (void)hipEventDestroy(pe.second.second);
+  }
+  for (auto e : a->prof_pool) (void)hipEventDestroy(e);
+  (void)hipFree(a->probe_flag);
+  delete a;
+  return ok();
+}
+
+kv_status kv_rebuild_stage(kv_arena_t arena, const int32_t* tokens, const int32_t* lens, int32_t R,
+                           const int32_t* tables, int32_t max_blocks, void* workspace,
+                           uint64_t ws_bytes, void* stream, kv_plan_t* out) {
+  if (!out) return fail(KV_EINVAL, "null output plan");
+  *out = nullptr;
+  if (!live_arena(arena)) return fail(KV_ESTATE, "unknown or released arena handle");
+  int64_t T = 0;
+  int32_t max_len = 0;
+  kv_status st = check_request(&arena->desc, arena->block_size, arena->num_blocks, tokens, lens, R,
+                               tables, max_blocks, &T, &max_len);
+  if (st != KV_OK) return st;
+  const kv_model_desc& d = arena->desc;
+  kv_plan* plan = new (std::nothrow) kv_plan();
+  if (!plan) return fail(KV_ENOMEM, "host allocation failed");
+  plan->arena = arena;
+  plan->ws = reinterpret_cast<char*>(workspace);
+  plan->ws_bytes = ws_bytes;
+  plan->max_len = max_len;
+  if (T > 0) {
+    if (!workspace) {
+      delete plan;
+      return fail(KV_EINVAL, "null workspace");
+    }
+    const Layout smallest = make_layout(d, R, T, max_len);
+    if (smallest.total > ws_bytes) {
+      delete plan;
+      return fail(KV_ENOMEM, "workspace of %llu bytes < %llu needed for the longest request",
+                  (unsigned long long)ws_bytes, (unsigned long long)smallest.total);
+    }
+    // largest wave capacity whose layout fits
+    int64_t lo = max_len, hi = T;
+    while (lo < hi) {
+      const int64_t mid = lo + (hi - lo + 1) / 2;
+      if (make_layout(d, R, T, mid).total <= ws_bytes) lo = mid; else hi = mid - 1;
+    }
+    plan->lay = make_layout(d, R, T, lo);
+    const Layout& L = plan->lay;
+
+    // waves: consecutive requests, never split
+    std::vector<int64_t> req_off(R + 1, 0);
+    for (int32_t r = 0; r < R; ++r) req_off[r + 1] = req_off[r] + lens[r];
+    {
+      Wave w{0, 0, 0, 0, 0.0};
+      for (int32_t r = 0; r < R; ++r) {
+        if (lens[r] == 0) continue;
+        if (w.rows > 0 && w.rows + (int64_t)lens[r] > L.W) {
+          plan->waves.push_back(w);
+          w = Wave{req_off[r], 0, 0, 0, 0.0};
+        }
+        if (w.rows == 0) w.tok_begin = req_off[r];
+        w.rows += lens[r];
+        w.causal_pairs += 0.5 * (double)lens[r] * ((double)lens[r] + 1.0);
+      }
+      if (w.rows > 0) plan->waves.push_back(w);
+    }
+
+    // metadata image in pinned host memory, then one async copy
+    if (arena->staged_pending) {
+      (void)hipEventSynchronize(arena->staged);
+      arena->staged_pending = false;
+    }
+    DeviceGuard dg(arena->device);
+    if (arena->pinned_bytes < L.meta_end) {
+      if (arena->pinned) (void)hipHostFree(arena->pinned);
+      arena->pinned = nullptr;
+      arena->pinned_bytes = 0;
+      if (hipHostMalloc(&arena->pinned, L.meta_end, hipHostMallocDefault) != hipSuccess) {
+        arena->pinned = nullptr;
+        delete plan;
+        return fail(KV_ENOMEM, "pinned staging allocation of %zu bytes failed", (size_t)L.meta_end);
+      }
+      arena->pinned_bytes = L.meta_end;
+    }
+    char* hb = reinterpret_cast<char*>(arena->pinned);
+    int32_t* htok = reinterpret_cast<int32_t*>(hb + L.tok);
+    int32_t* hpos = reinterpret_cast<int32_t*>(hb + L.pos);
+    int64_t* hslot = reinterpret_cast<int64_t*>(hb + L.slot);
+    int4* hq = reinterpret_cast<int4*>(hb + L.qblk);
+    std::memcpy(htok, tokens, sizeof(int32_t) * (size_t)T);
+    const int32_t B = arena->block_size;
+    for (int32_t r = 0; r < R; ++r) {
+      const int32_t* tab = tables + (int64_t)r * max_blocks;
+      for (int32_t p = 0; p < lens[r]; ++p) {
+        const int64_t t = req_off[r] + p;
+        hpos[t] = p;
+        hslot[t] = (int64_t)tab[p / B] * B + p % B;
+      }
+    }
+    int32_t nq_total = 0;
+    for (auto& w : plan->waves) {
+      w.qblk_begin = nq_total;
+      std::vector<int4> blocks;
+      for (int32_t r = 0; r < R; ++r) {
+        if (lens[r] == 0 || req_off[r] < w.tok_begin || req_off[r] >= w.tok_begin + w.rows) continue;
+        const int32_t rs = (int32_t)(req_off[r] - w.tok_begin);
+        for (int32_t qs = 0; qs < lens[r]; qs += ATTN_QBLOCK)
+          blocks.push_back(make_int4(rs + qs, std::min(ATTN_QBLOCK, lens[r] - qs), rs, 0));
+      }
+      // longest causal extent first
+      std::stable_sort(blocks.begin(), blocks.end(), [](const int4& x, const int4& y) {
+        return (x.x + x.y - x.z) > (y.x + y.y - y.z);
+      });
+      std::memcpy(hq + nq_total, blocks.data(), sizeof(int4) * blocks.size());
+      w.num_qblk = (int32_t)blocks.size();
+      nq_total += w.num_qblk;
+    }
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(plan->ws, hb, L.meta_end, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipEventRecord(arena->staged, s);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      delete plan;
+      return fail(KV_EDEVICE, "metadata upload failed: %s", hipGetErrorString(e));
+    }
+    arena->staged_pending = true;
+  }
+  {
+    std::lock_guard<std::mutex> g(g_reg_mu);
+    g_plans.insert(plan);
+  }
+  *out = plan;
+  return ok();
+}
+
+kv_status kv_plan_release(kv_plan_t plan) {
+  {
+    std::lock_guard<std::mutex> g(g_reg_mu);
+    if (!plan || !g_plans.count(plan)) return fail(KV_ESTATE, "unknown or released plan");
+    g_plans.erase(plan);
+  }
+  delete plan;
+  return ok();
+}
+
+kv_status kv_plan_info(kv_plan_t plan, int32_t* num_waves, int64_t* max_wave_tokens) {
+  if (!live_plan(plan)) return fail(KV_ESTATE, "unknown or released plan");
+  int64_t mx = 0;
+  for (auto& w : plan->waves) mx = std::max<int64_t>(mx, w.rows);
+  if (num_waves) *num_waves = (int32_t)plan->waves.size();
+  if (max_wave_tokens) *max_wave_tokens = mx;
+  return ok();
+}
+
+kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) {
+  if (!live_plan(plan)) return fail(KV_ESTATE, "unknown or released plan");
+  kv_arena* ar = plan->arena;
+  if (!live_arena(ar)) return fail(KV_ESTATE, "the plan's arena was released");
+  if (!w || !w->embed || !w->layers) return fail(KV_EINVAL, "null weights");
+  const kv_model_desc& d = ar->desc;
+  if (!same_desc(w->desc, d)) return fail(KV_ESTATE, "weights and arena describe different models");
+  for (int l = 0; l < d.num_layers; ++l) {
+    const kv_layer_weights& lw = w->layers[l];
+    if (!lw.attn_norm || !lw.wq || !lw.wk || !lw.wv || !lw.wo || !lw.ffn_norm || !lw.w_gate ||
+        !lw.w_up || !lw.w_down)
+      return fail(KV_EINVAL, "null weight pointer in layer %d", l);
+  }
+  if (plan->waves.empty()) return ok();
+  DeviceGuard dg(ar->device);
+  if (dg.err != hipSuccess) return fail(KV_EDEVICE, "cannot select device %d", ar->device);
+  {
+    const hipError_t pre = hipGetLastError();
+    if (pre != hipSuccess) return fail(KV_EDEVICE, "pending device error: %s", hipGetErrorString(pre));
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const Layout& L = plan->lay;
+  char* ws = plan->ws;
+  const int dt = d.dtype;
+  const int64_t e = elem_bytes(dt);
+  const int H = d.hidden, nq = d.num_q_heads, nkv = d.num_kv_heads, hd = d.head_dim, F = d.ffn_dim;
+  const float eps = (float)d.rms_eps;
+  const int64_t plane = ar->num_blocks * (int64_t)ar->block_size * nkv * hd;  // elements
+  char* abase = reinterpret_cast<char*>(ar->base);
+  float2* rope = reinterpret_cast<float2*>(ws + L.rope);
+  float* X = reinterpret_cast<float*>(ws + L.x);
+  void* A = ws + L.a;
+  void* Q = ws + L.q;
+  void* U = ws + L.u;
+  void* VT = dt == KV_BF16 ? (void*)(ws + L.vt) : nullptr;
+  void* HF = ws + L.hf;
+  auto gemm = dt == KV_BF16 ? launch_gemm_bf16 : launch_gemm_f32;
+
+  {
+    ProfScope ps(ar, s, KV_PROF_ROPE, 0.0);
+    launch_rope_table(rope, plan->max_len, hd, d.rope_theta, s);
+  }
+  for (const Wave& wv : plan->waves) {
+    const int M = wv.rows;
+    const int32_t* tok = reinterpret_cast<const int32_t*>(ws + L.tok) + wv.tok_begin;
+    const int32_t* pos = reinterpret_cast<const int32_t*>(ws + L.pos) + wv.tok_begin;
+    const int64_t* slot = reinterpret_cast<const int64_t*>(ws + L.slot) + wv.tok_begin;
+    const int4* qblk = reinterpret_cast<const int4*>(ws + L.qblk) + wv.qblk_begin;
+    {
+      ProfScope ps(ar, s, KV_PROF_NORM, 0.0);
+      launch_embed_norm(dt, w->embed, tok, w->layers[0].attn_norm, X, A, M, H, eps, s);
+    }
+    for (int l = 0; l < d.num_layers; ++l) {
+      const kv_layer_weights& lw = w->layers[l];
+      const bool last = l == d.num_layers - 1;
+      if (l > 0) {
+        ProfScope ps(ar, s, KV_PROF_NORM, 0.0);
+        launch_rmsnorm(dt, X, lw.attn_norm, A, M, H, eps, s);
+      }
+      char* plane_k = abase + (int64_t)(2 * l) * plane * e;
+      char* plane_v = abase + (int64_t)(2 * l + 1) * plane * e;
+
+      GemmParams g{};
+      g.A = A;
+      g.lda = H;
+      g.M = M;
+      g.K = H;
+      g.B0 = lw.wq;
+      g.B1 = lw.wk;
+      g.B2 = lw.wv;
+      g.bmap = BMAP_QKV;
+      g.s0 = nq * hd;
+      g.s1 = nq * hd + nkv * hd;
+      g.n_begin = last ? nq * hd : 0;
+      g.n_end = (nq + 2 * nkv) * hd;
+      g.epi.q_out = Q;
+      g.epi.arena_k = plane_k;
+      g.epi.arena_v = plane_v;
+      g.epi.vt = VT;
+      g.epi.ldvt = L.Wpad;
+      g.epi.slot = slot;
+      g.epi.pos = pos;
+      g.epi.rope = rope;
+      g.epi.nq = nq;
+      g.epi.nkv = nkv;
+      g.epi.d = hd;
+      {
+        ProfScope ps(ar, s, KV_PROF_GEMM_QKV, 2.0 * M * (double)(g.n_end - g.n_begin) * H);
+        gemm(EPI_QKV, g, s);
+      }
+      if (last) break;
+
+      AttnParams ap{};
+      ap.q = Q;
+      ap.arena_k = plane_k;
+      ap.arena_v = plane_v;
+      ap.vt = VT;
+      ap.ldvt = L.Wpad;
+      ap.slot = slot;
+      ap.qblk = qblk;
+      ap.num_qblk = wv.num_qblk;
+      ap.out = U;
+      ap.nq = nq;
+      ap.nkv = nkv;
+      ap.d = hd;
+      {
+        // causal-triangle flops: QK^T and PV over the visible (query, key) pairs
+        ProfScope ps(ar, s, KV_PROF_ATTN, 4.0 * nq * hd * wv.causal_pairs);
+        if (dt == KV_BF16) launch_attention_bf16(ap, s); else launch_attention_f32(ap, M, s);
+      }
+
+      GemmParams go{};
+      go.A = U;
+      go.lda = nq * hd;
+      go.M = M;
+      go.K = nq * hd;
+      go.B0 = lw.wo;
+      go.bmap = BMAP_PLAIN;
+      go.n_begin = 0;
+      go.n_end = H;
+      go.epi.x = X;
+      go.epi.ldx = H;
+      {
+        ProfScope ps(ar, s, KV_PROF_GEMM_O, 2.0 * M * (double)H * nq * hd);
+        gemm(EPI_RESID, go, s);
+      }
+      {
+        ProfScope ps(ar, s, KV_PROF_NORM, 0.0);
+        launch_rmsnorm(dt, X, lw.ffn_norm, A, M, H, eps, s);
+      }
+      GemmParams gu{};
+      gu.A = A;
+      gu.lda = H;
+      gu.M = M;
+      gu.K = H;
+      gu.B0 = lw.w_gate;
+      gu.B1 = lw.w_up;
+      gu.bmap = BMAP_GATEUP;
+      gu.n_begin = 0;
+      gu.n_end = 2 * F;
+      gu.epi.hf = HF;
+      gu.epi.ldh = F;
+      gu.epi.ffn = F;
+      {
+        ProfScope ps(ar, s, KV_PROF_GEMM_GATEUP, 2.0 * M * 2.0 * F * H);
+        gemm(EPI_SWIGLU, gu, s);
+      }
+      GemmParams gd{};
+      gd.A = HF;
+      gd.lda = F;
+      gd.M = M;
+      gd.K = F;
+      gd.B0 = lw.w_down;
+      gd.bmap = BMAP_PLAIN;
+      gd.n_begin = 0;
+      gd.n_end = H;
+      gd.epi.x = X;
+      gd.epi.ldx = H;
+      {
+        ProfScope ps(ar, s, KV_PROF_GEMM_DOWN, 2.0 * M * (double)H * F);
+        gemm(EPI_RESID, gd, s);
+      }
+    }
+  }
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(KV_EDEVICE, "kernel launch failed: %s", hipGetErrorString(err));
+  return ok();
+}
+
+kv_status kv_rebuild(const kv_weights* w, const int32_t* tokens, const int32_t* lens, int32_t R,
+                     const int32_t* tables, int32_t max_blocks, kv_arena_t arena, void* workspace,
+                     uint64_t ws_bytes, void* stream) {
+  if (!w) return fail(KV_EINVAL, "null weights");
+  if (!live_arena(arena)) return fail(KV_ESTATE, "unknown or released arena handle");
+  if (!same_desc(w->desc, arena->desc)) return fail(KV_ESTATE, "weights and arena describe different models");
+  kv_plan_t plan = nullptr;
+  kv_status st = kv_rebuild_stage(arena, tokens, lens, R, tables, max_blocks, workspace, ws_bytes,
+                                  stream, &plan);
+  if (st != KV_OK) return st;
+  st = kv_rebuild_execute(w, plan, stream);
+  const std::string keep = g_err;
+  kv_plan_release(plan);
+  if (st != KV_OK) {
+    g_err = keep;
+    return st;
+  }
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// Per-kernel-class timing (kvr_profile.h)
+// ---------------------------------------------------------------------------
+kv_status kv_profile_enable(kv_arena_t a, int32_t enable) {
+  if (!live_arena(a)) return fail(KV_ESTATE, "unknown or released arena handle");
+  a->profile = enable != 0;
+  return ok();
+}
+
+kv_status kv_profile_read(kv_arena_t a, double* ms, int64_t* launches, double* flops,
+                          int32_t n_classes) {
+  if (!live_arena(a)) return fail(KV_ESTATE, "unknown or released arena handle");
+  DeviceGuard dg(a->device);
+  size_t fi = 0;
+  for (auto& pe : a->prof_pending) {
+    float t = 0.0f;
+    (void)hipEventSynchronize(pe.second.second);
+    (void)hipEventElapsedTime(&t, pe.second.first, pe.second.second);
+    a->prof_ms[pe.first] += t;
+    a->prof_launches[pe.first] += 1;
+    a->prof_flops[pe.first] += fi < a->pending_flops.size() ? a->pending_flops[fi] : 0.0;
+    ++fi;
+    a->prof_pool.push_back(pe.second.first);
+    a->prof_pool.push_back(pe.second.second);
+  }
+  a->prof_pending.clear();
+  a->pending_flops.clear();
+  for (int32_t c = 0; c < n_classes && c < KV_PROF_CLASSES; ++c) {
+    if (ms) ms[c] = a->prof_ms[c];
+    if (launches) launches[c] = a->prof_launches[c];
+    if (flops) flops[c] = a->prof_flops[c];
+  }
+  return ok();
+}
+
+kv_status kv_profile_reset(kv_arena_t a) {
+  if (!live_arena(a)) return fail(KV_ESTATE, "unknown or released arena handle");
+  double tmp[KV_PROF_CLASSES];
+  kv_status st = kv_profile_read(a, tmp, nullptr, nullptr, KV_PROF_CLASSES);
+  if (st != KV_OK) return st;
+  for (int c = 0; c < KV_PROF_CLASSES; ++c) {
+    a->prof_ms[c] = 0.0;
+    a->prof_launches[c] = 0;
+    a->prof_flops[c] = 0.0;
+  }
+  return ok();
+}
+
+}  // extern "C"

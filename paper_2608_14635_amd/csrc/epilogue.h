@@ -1,0 +1,136 @@
+// Fused GEMM epilogues, shared by the bf16 MFMA GEMM and the fp32 GEMM.
+//
+// A tile's fp32 accumulators are first parked in LDS as sC[rows][ldc]; the
+// routines below then read it in row-contiguous chunks so that every global
+// store is a full 16-byte (bf16) or 32-byte (fp32) vector:
+//   QKV    : NeoX RoPE on the q and k heads of the tile (pairs (i, i+d/2),
+//            fp32 cos/sin from the per-position table), rounding to the model
+//            dtype, Q rows to the workspace, K and V rows scattered to their
+//            arena slots, and V^T columns for the attention kernel;
+//   RESID  : X += acc on the fp32 residual stream;
+//   SWIGLU : h = silu(gate) * up from the two column halves of the tile.
+#pragma once
+#include "common.h"
+#include "launch.h"
+
+namespace kvr {
+
+// QKV: the tile covers logical columns [n0, n0+BN) lying in one region
+// (q: [0, nq*d), k: [nq*d, nq*d + nkv*d), v: after that) and BN % d == 0.
+template <typename T, int BN, int NT>
+__device__ __forceinline__ void epi_qkv(const float* sC, int ldc, int rows, int m_base, int M,
+                                        int n0, const EpiParams& e) {
+  const int tid = threadIdx.x;
+  const int d = e.d, half = d >> 1;
+  const int qcols = e.nq * d, kcols = e.nkv * d;
+  const int region = n0 < qcols ? 0 : (n0 < qcols + kcols ? 1 : 2);
+  if (region < 2) {
+    // items: (row, head in tile, chunk of 8 rotary pairs)
+    const int heads = BN / d, chunks = half / 8;
+    const int per_row = heads * chunks;
+    for (int it = tid; it < rows * per_row; it += NT) {
+      const int r = it / per_row, hc = it % per_row;
+      const int hh = hc / chunks, c0 = (hc % chunks) * 8;
+      const int m = m_base + r;
+      if (m >= M) continue;
+      const float* src = sC + (int64_t)r * ldc + hh * d;
+      const int p = e.pos[m];
+      const float2* cs = e.rope + (int64_t)p * half + c0;
+      float lo[8], hi[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float a = src[c0 + i], b = src[c0 + half + i];
+        const float2 t = cs[i];
+        lo[i] = Elem<T>::round(a * t.x - b * t.y);
+        hi[i] = Elem<T>::round(b * t.x + a * t.y);
+      }
+      T* dst;
+      if (region == 0) {
+        dst = reinterpret_cast<T*>(e.q_out) + (int64_t)m * qcols + n0 + hh * d;
+      } else {
+        const int kh = (n0 - qcols) / d + hh;
+        dst = reinterpret_cast<T*>(e.arena_k) + (e.slot[m] * e.nkv + kh) * (int64_t)d;
+      }
+      store8(dst + c0, lo);
+      store8(dst + c0 + half, hi);
+    }
+  } else {
+    const int vbase = n0 - qcols - kcols;  // first V column (head-major) of the tile
+    const int per_row = BN / 8;
+    for (int it = tid; it < rows * per_row; it += NT) {
+      const int r = it / per_row, c0 = (it % per_row) * 8;
+      const int m = m_base + r;
+      if (m >= M) continue;
+      const float* src = sC + (int64_t)r * ldc + c0;
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = src[i];
+      const int col = vbase + c0;  // = kh * d + e
+      T* dst = reinterpret_cast<T*>(e.arena_v) + e.slot[m] * (int64_t)kcols + col;
+      store8(dst, v);
+    }
+    if (e.vt != nullptr) {
+      // V^T[kh][e][m]: 8 consecutive rows of one column per item; the buffer is
+      // padded to whole tiles, so rows >= M are written (and never read).
+      const int rchunks = rows / 8;
+      for (int it = tid; it < BN * rchunks; it += NT) {
+        const int c = it % BN, rc = it / BN;
+        const float* src = sC + (int64_t)(rc * 8) * ldc + c;
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = src[(int64_t)i * ldc];
+        const int col = vbase + c;
+        T* dst = reinterpret_cast<T*>(e.vt) + (int64_t)col * e.ldvt + m_base + rc * 8;
+        store8(dst, v);
+      }
+    }
+  }
+}
+
+template <int BN, int NT>
+__device__ __forceinline__ void epi_resid(const float* sC, int ldc, int rows, int m_base, int M,
+                                          int n0, const EpiParams& e) {
+  const int tid = threadIdx.x;
+  const int per_row = BN / 4;
+  for (int it = tid; it < rows * per_row; it += NT) {
+    const int r = it / per_row, c0 = (it % per_row) * 4;
+    const int m = m_base + r;
+    if (m >= M) continue;
+    float4* xp = reinterpret_cast<float4*>(e.x + (int64_t)m * e.ldx + n0 + c0);
+    const float* src = sC + (int64_t)r * ldc + c0;
+    float4 xv = *xp;
+    xv.x += src[0];
+    xv.y += src[1];
+    xv.z += src[2];
+    xv.w += src[3];
+    *xp = xv;
+  }
+}
+
+// SWIGLU: tile columns [0, BN/2) are gate rows j0.., [BN/2, BN) the same up rows.
+template <typename T, int BN, int NT>
+__device__ __forceinline__ void epi_swiglu(const float* sC, int ldc, int rows, int m_base, int M,
+                                           int j0, const EpiParams& e) {
+  const int tid = threadIdx.x;
+  constexpr int HB = BN / 2;
+  const int per_row = HB / 8;
+  for (int it = tid; it < rows * per_row; it += NT) {
+    const int r = it / per_row, c0 = (it % per_row) * 8;
+    const int m = m_base + r;
+    if (m >= M || j0 + c0 >= e.ffn) continue;
+    const float* src = sC + (int64_t)r * ldc + c0;
+    float h[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = Elem<T>::round(silu(src[i]) * src[HB + i]);
+    T* dst = reinterpret_cast<T*>(e.hf) + (int64_t)m * e.ldh + j0 + c0;
+    if (j0 + c0 + 8 <= e.ffn) {
+      store8(dst, h);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (j0 + c0 + i < e.ffn) Elem<T>::store(dst, i, h[i]);
+    }
+  }
+}
+
+}  // namespace kvr

@@ -1,0 +1,85 @@
+// Kernel launch interface between the host planner (abi.cpp) and the device
+// code.  Plain structs of device pointers and sizes; no HIP types beyond
+// hipStream_t.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kvr {
+
+enum Epi : int {
+  EPI_QKV = 0,     // RoPE on q/k; Q -> workspace, K/V -> arena slots (+ V^T for attention)
+  EPI_RESID = 1,   // X += acc (fp32 residual stream)
+  EPI_SWIGLU = 2,  // Hf = silu(gate) * up
+};
+
+enum BMap : int {
+  BMAP_PLAIN = 0,   // B rows n of one matrix
+  BMAP_QKV = 1,     // rows [0,s0) of Wq, [s0,s1) of Wk, [s1,..) of Wv
+  BMAP_GATEUP = 2,  // tile of BN rows = BN/2 rows of W_gate then the same BN/2 rows of W_up
+};
+
+struct EpiParams {
+  // QKV
+  void* q_out;            // [rows][nq*d]
+  void* arena_k;          // this layer's K plane: [slots][nkv][d]
+  void* arena_v;          // this layer's V plane
+  void* vt;               // V^T [nkv][d][ldvt] (bf16 path) or null
+  int64_t ldvt;
+  const int64_t* slot;    // per wave-local token: arena slot index
+  const int32_t* pos;     // per wave-local token: position within its request
+  const float2* rope;     // [max_pos][d/2] (cos, sin)
+  int nq, nkv, d;
+  // RESID
+  float* x;               // [rows][ldx]
+  int ldx;
+  // SWIGLU
+  void* hf;               // [rows][ldh]
+  int ldh;
+  int ffn;
+};
+
+struct GemmParams {
+  const void* A;          // [M][K] activations, K contiguous
+  int64_t lda;
+  int M, K;
+  const void* B0;         // weights [.][K] rows, K contiguous
+  const void* B1;
+  const void* B2;
+  int bmap;
+  int s0, s1;             // BMAP_QKV split points (logical columns)
+  int n_begin, n_end;     // logical column range of C computed by this launch
+  EpiParams epi;
+};
+
+// Elementwise / small kernels
+void launch_rope_table(float2* table, int max_pos, int d, double theta, hipStream_t s);
+void launch_embed_norm(int dtype, const void* embed, const int32_t* tok, const void* gain,
+                       float* x, void* a_out, int rows, int hidden, float eps, hipStream_t s);
+void launch_rmsnorm(int dtype, const float* x, const void* gain, void* a_out, int rows,
+                    int hidden, float eps, hipStream_t s);
+int launch_probe(int* dev_flag, hipStream_t s);
+
+// GEMMs with fused epilogues
+void launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s);
+void launch_gemm_f32(int epi, const GemmParams& p, hipStream_t s);
+
+// Attention.  qblk: per q-block int4 {q_start, q_len, req_start, 0} in wave-local
+// token indices, ordered longest-first.
+struct AttnParams {
+  const void* q;          // [rows][nq*d]
+  const void* arena_k;    // this layer's K plane
+  const void* arena_v;    // this layer's V plane (fp32 path)
+  const void* vt;         // V^T [nkv][d][ldvt] (bf16 path)
+  int64_t ldvt;
+  const int64_t* slot;
+  const int4* qblk;
+  int num_qblk;
+  void* out;              // [rows][nq*d]
+  int nq, nkv, d;
+};
+constexpr int ATTN_QBLOCK = 128;  // queries per q-block (bf16 path)
+void launch_attention_bf16(const AttnParams& p, hipStream_t s);
+void launch_attention_f32(const AttnParams& p, int rows_total, hipStream_t s);
+
+}  // namespace kvr

@@ -1,0 +1,224 @@
+"""Thin ctypes binding of libkvr.so (include/kvr.h, include/kvr_profile.h).
+
+Argument marshalling only: every step of the rebuild runs in the library's
+HIP kernels.  Device buffers are passed as integer addresses (for example a
+torch tensor's data_ptr()), host arrays as numpy int32 arrays, streams as the
+integer value of a hipStream_t (torch.cuda.Stream.cuda_stream).  Errors raise
+KvError carrying the library's status code and message.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Dict, Iterable, Optional, Sequence, Tuple
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libkvr.so")
+
+KV_OK, KV_EINVAL, KV_ERANGE, KV_EALIAS, KV_ECAPACITY, KV_EDEVICE, KV_ENOMEM, KV_ESTATE = \
+    0, -1, -2, -3, -4, -5, -6, -7
+STATUS_NAMES = {0: "KV_OK", -1: "KV_EINVAL", -2: "KV_ERANGE", -3: "KV_EALIAS", -4: "KV_ECAPACITY",
+                -5: "KV_EDEVICE", -6: "KV_ENOMEM", -7: "KV_ESTATE"}
+KV_F32, KV_BF16 = 0, 1
+PROF_CLASSES = ("rope", "norm", "gemm_qkv", "attention", "gemm_o", "gemm_gateup", "gemm_down")
+LAYER_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
+
+
+class KvError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class kv_model_desc(C.Structure):
+    _fields_ = [("num_layers", C.c_int32), ("hidden", C.c_int32), ("num_q_heads", C.c_int32),
+                ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn_dim", C.c_int32),
+                ("vocab", C.c_int32), ("rms_eps", C.c_double), ("rope_theta", C.c_double),
+                ("dtype", C.c_int32)]
+
+
+class kv_layer_weights(C.Structure):
+    _fields_ = [(k, C.c_void_p) for k in LAYER_FIELDS]
+
+
+class kv_weights(C.Structure):
+    _fields_ = [("desc", kv_model_desc), ("embed", C.c_void_p),
+                ("layers", C.POINTER(kv_layer_weights))]
+
+
+_lib: Optional[C.CDLL] = None
+
+
+def lib() -> C.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2608_14635_amd.build` (there is no fallback path)")
+    L = C.CDLL(LIB_PATH)
+    i32p = C.POINTER(C.c_int32)
+    vp = C.c_void_p
+    L.kv_last_error.restype = C.c_char_p
+    L.kv_rebuild_workspace_bytes.restype = C.c_uint64
+    L.kv_rebuild_workspace_bytes.argtypes = [C.POINTER(kv_model_desc), C.c_int32, C.c_int64, C.c_int64]
+    L.kv_rebuild_check.restype = C.c_int
+    L.kv_rebuild_check.argtypes = [C.POINTER(kv_model_desc), C.c_int32, C.c_int64, i32p, i32p,
+                                   C.c_int32, i32p, C.c_int32]
+    L.kv_arena_bind.restype = C.c_int
+    L.kv_arena_bind.argtypes = [vp, C.c_uint64, C.POINTER(kv_model_desc), C.c_int32, C.c_int64,
+                                C.c_int32, C.POINTER(vp)]
+    L.kv_arena_release.restype = C.c_int
+    L.kv_arena_release.argtypes = [vp]
+    L.kv_rebuild.restype = C.c_int
+    L.kv_rebuild.argtypes = [C.POINTER(kv_weights), i32p, i32p, C.c_int32, i32p, C.c_int32, vp,
+                             vp, C.c_uint64, vp]
+    L.kv_rebuild_stage.restype = C.c_int
+    L.kv_rebuild_stage.argtypes = [vp, i32p, i32p, C.c_int32, i32p, C.c_int32, vp, C.c_uint64, vp,
+                                   C.POINTER(vp)]
+    L.kv_rebuild_execute.restype = C.c_int
+    L.kv_rebuild_execute.argtypes = [C.POINTER(kv_weights), vp, vp]
+    L.kv_plan_release.restype = C.c_int
+    L.kv_plan_release.argtypes = [vp]
+    L.kv_plan_info.restype = C.c_int
+    L.kv_plan_info.argtypes = [vp, C.POINTER(C.c_int32), C.POINTER(C.c_int64)]
+    L.kv_profile_enable.restype = C.c_int
+    L.kv_profile_enable.argtypes = [vp, C.c_int32]
+    L.kv_profile_read.restype = C.c_int
+    L.kv_profile_read.argtypes = [vp, C.POINTER(C.c_double), C.POINTER(C.c_int64),
+                                  C.POINTER(C.c_double), C.c_int32]
+    L.kv_profile_reset.restype = C.c_int
+    L.kv_profile_reset.argtypes = [vp]
+    _lib = L
+    return L
+
+
+def kv_last_error() -> str:
+    return lib().kv_last_error().decode()
+
+
+def _check(st: int) -> None:
+    if st != KV_OK:
+        raise KvError(st, kv_last_error())
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(C.POINTER(C.c_int32)) if a.size else None
+
+
+def make_desc(shape) -> kv_model_desc:
+    """kv_model_desc from any object with the ModelShape fields."""
+    return kv_model_desc(shape.num_layers, shape.hidden, shape.num_q_heads, shape.num_kv_heads,
+                         shape.head_dim, shape.ffn_dim, shape.vocab, float(shape.rms_eps),
+                         float(shape.rope_theta), int(shape.dtype))
+
+
+class Weights:
+    """Owns the ctypes kv_weights struct and its host layer array."""
+
+    def __init__(self, desc: kv_model_desc, embed_ptr: int, layer_ptrs: Sequence[Dict[str, int]]):
+        self._layers = (kv_layer_weights * len(layer_ptrs))()
+        for i, lp in enumerate(layer_ptrs):
+            for k in LAYER_FIELDS:
+                setattr(self._layers[i], k, lp[k])
+        self.c = kv_weights(desc, embed_ptr, C.cast(self._layers, C.POINTER(kv_layer_weights)))
+
+
+def _tables2d(tables, n_req: int) -> Tuple[np.ndarray, int]:
+    t = _i32(tables)
+    if t.ndim != 2:
+        t = t.reshape(n_req, -1) if n_req else t.reshape(0, 0)
+    return t, int(t.shape[1]) if t.ndim == 2 else 0
+
+
+def kv_rebuild_workspace_bytes(shape_or_desc, num_requests: int, total_tokens: int,
+                               wave_tokens: int) -> int:
+    d = shape_or_desc if isinstance(shape_or_desc, kv_model_desc) else make_desc(shape_or_desc)
+    return int(lib().kv_rebuild_workspace_bytes(C.byref(d), num_requests, total_tokens, wave_tokens))
+
+
+def kv_rebuild_check(shape_or_desc, block_size: int, num_blocks: int, tokens, lens, tables) -> int:
+    """Host-only validation; returns the status code (no exception)."""
+    d = shape_or_desc if isinstance(shape_or_desc, kv_model_desc) else make_desc(shape_or_desc)
+    tok, ln = _i32(tokens), _i32(lens)
+    tab, mb = _tables2d(tables, len(ln))
+    return int(lib().kv_rebuild_check(C.byref(d), block_size, num_blocks, _ptr(tok), _ptr(ln),
+                                      len(ln), _ptr(tab), mb))
+
+
+def kv_arena_bind(base: int, nbytes: int, shape_or_desc, block_size: int, num_blocks: int,
+                  device: int = 0) -> int:
+    d = shape_or_desc if isinstance(shape_or_desc, kv_model_desc) else make_desc(shape_or_desc)
+    h = C.c_void_p()
+    _check(lib().kv_arena_bind(C.c_void_p(base), nbytes, C.byref(d), block_size, num_blocks,
+                               device, C.byref(h)))
+    return h.value
+
+
+def kv_arena_release(arena: int) -> None:
+    _check(lib().kv_arena_release(C.c_void_p(arena)))
+
+
+def kv_rebuild(weights: Weights, tokens, lens, tables, arena: int, workspace: int,
+               workspace_bytes: int, stream: int = 0) -> None:
+    tok, ln = _i32(tokens), _i32(lens)
+    tab, mb = _tables2d(tables, len(ln))
+    _check(lib().kv_rebuild(C.byref(weights.c), _ptr(tok), _ptr(ln), len(ln), _ptr(tab), mb,
+                            C.c_void_p(arena), C.c_void_p(workspace), workspace_bytes,
+                            C.c_void_p(stream)))
+
+
+def kv_rebuild_stage(arena: int, tokens, lens, tables, workspace: int, workspace_bytes: int,
+                     stream: int = 0) -> int:
+    tok, ln = _i32(tokens), _i32(lens)
+    tab, mb = _tables2d(tables, len(ln))
+    plan = C.c_void_p()
+    _check(lib().kv_rebuild_stage(C.c_void_p(arena), _ptr(tok), _ptr(ln), len(ln), _ptr(tab), mb,
+                                  C.c_void_p(workspace), workspace_bytes, C.c_void_p(stream),
+                                  C.byref(plan)))
+    return plan.value
+
+
+def kv_rebuild_execute(weights: Weights, plan: int, stream: int = 0) -> None:
+    _check(lib().kv_rebuild_execute(C.byref(weights.c), C.c_void_p(plan), C.c_void_p(stream)))
+
+
+def kv_plan_release(plan: int) -> None:
+    _check(lib().kv_plan_release(C.c_void_p(plan)))
+
+
+def kv_plan_info(plan: int) -> Tuple[int, int]:
+    nw, mx = C.c_int32(), C.c_int64()
+    _check(lib().kv_plan_info(C.c_void_p(plan), C.byref(nw), C.byref(mx)))
+    return nw.value, mx.value
+
+
+def kv_profile_enable(arena: int, enable: bool = True) -> None:
+    _check(lib().kv_profile_enable(C.c_void_p(arena), 1 if enable else 0))
+
+
+def kv_profile_read(arena: int) -> Dict[str, Dict[str, float]]:
+    n = len(PROF_CLASSES)
+    ms, la, fl = (C.c_double * n)(), (C.c_int64 * n)(), (C.c_double * n)()
+    _check(lib().kv_profile_read(C.c_void_p(arena), ms, la, fl, n))
+    return {name: {"ms": ms[i], "launches": int(la[i]), "flops": fl[i]}
+            for i, name in enumerate(PROF_CLASSES)}
+
+
+def kv_profile_reset(arena: int) -> None:
+    _check(lib().kv_profile_reset(C.c_void_p(arena)))
+
+
+def exported_symbols() -> Iterable[str]:
+    return ("kv_arena_bind", "kv_arena_release", "kv_rebuild_workspace_bytes", "kv_rebuild_check",
+            "kv_rebuild", "kv_rebuild_stage", "kv_rebuild_execute", "kv_plan_release",
+            "kv_plan_info", "kv_last_error", "kv_profile_enable", "kv_profile_read",
+            "kv_profile_reset")

@@ -1,0 +1,173 @@
+"""C-ABI library checks that need no GPU: it loads, exports every function
+the headers declare, sizes workspaces, and rejects invalid requests with the
+documented status codes before touching any device."""
+import ctypes as C
+import dataclasses
+import glob
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_14635_amd import kvr
+from paper_2608_14635_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(kvr.LIB_PATH):
+        from paper_2608_14635_amd import build
+        build.build()
+    return kvr.lib()
+
+
+def declared_functions():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names.update(re.findall(r"\b(kv_[a-z_]+)\s*\(", text))
+    return sorted(names)
+
+
+def test_exports_every_declared_function(L):
+    decl = declared_functions()
+    assert len(decl) >= 13
+    for name in decl:
+        assert hasattr(L, name), f"{name} declared but not exported"
+    assert set(decl) == set(kvr.exported_symbols())
+
+
+def test_workspace_bytes(L):
+    s = W.LLAMA8B
+    assert kvr.kv_rebuild_workspace_bytes(dataclasses.replace(s, head_dim=64), 4, 1000, 1000) == 0
+    a = kvr.kv_rebuild_workspace_bytes(s, 16, 100000, 16384)
+    b = kvr.kv_rebuild_workspace_bytes(s, 16, 100000, 65536)
+    c = kvr.kv_rebuild_workspace_bytes(s, 16, 200000, 65536)
+    assert 0 < a < b < c
+    # activations dominate: fp32 residual + bf16 buffers per wave token
+    per_tok = 4 * s.hidden + 2 * (s.hidden + 2 * s.num_q_heads * s.head_dim + s.ffn_dim)
+    assert b >= 65536 * per_tok
+
+
+def _valid(shape=W.TINY_BF16, lens=(5, 16, 33), B=16, NB=20, seed=0):
+    rng = np.random.default_rng(seed)
+    lens = np.array(lens, np.int32)
+    toks = rng.integers(0, shape.vocab, size=int(lens.sum())).astype(np.int32)
+    need = (lens + B - 1) // B
+    perm = rng.permutation(NB).astype(np.int32)
+    tables = np.full((len(lens), int(need.max())), -1, np.int32)
+    o = 0
+    for r, k in enumerate(need):
+        tables[r, :k] = perm[o:o + k]
+        o += k
+    return shape, B, NB, toks, lens, tables
+
+
+def test_check_accepts_valid(L):
+    s, B, NB, toks, lens, tables = _valid()
+    assert kvr.kv_rebuild_check(s, B, NB, toks, lens, tables) == kvr.KV_OK
+
+
+@pytest.mark.parametrize("case,expect", [
+    ("token_high", kvr.KV_ERANGE), ("token_negative", kvr.KV_ERANGE),
+    ("block_high", kvr.KV_ERANGE), ("block_negative", kvr.KV_ERANGE),
+    ("alias_within", kvr.KV_EALIAS), ("alias_across", kvr.KV_EALIAS),
+    ("capacity", kvr.KV_ECAPACITY), ("negative_len", kvr.KV_EINVAL),
+    ("bad_shape", kvr.KV_EINVAL), ("zero_blocks", kvr.KV_EINVAL),
+])
+def test_check_errors(L, case, expect):
+    s, B, NB, toks, lens, tables = _valid()
+    toks, lens, tables = toks.copy(), lens.copy(), tables.copy()
+    if case == "token_high":
+        toks[7] = s.vocab
+    elif case == "token_negative":
+        toks[0] = -1
+    elif case == "block_high":
+        tables[2, 1] = NB
+    elif case == "block_negative":
+        tables[1, 0] = -5
+    elif case == "alias_within":
+        tables[2, 2] = tables[2, 0]
+    elif case == "alias_across":
+        tables[2, 0] = tables[0, 0]
+    elif case == "capacity":
+        tables = tables[:, :2]
+    elif case == "negative_len":
+        lens[1] = -1
+    elif case == "bad_shape":
+        s = dataclasses.replace(s, head_dim=64)
+    elif case == "zero_blocks":
+        NB = 0
+    assert kvr.kv_rebuild_check(s, B, NB, toks, lens, tables) == expect
+    assert kvr.kv_last_error() != ""
+
+
+def test_check_ignores_unused_table_entries(L):
+    s, B, NB, toks, lens, tables = _valid()
+    wide = np.full((tables.shape[0], tables.shape[1] + 3), 10 ** 6, np.int32)
+    wide[:, :tables.shape[1]] = tables
+    need = (lens + B - 1) // B
+    for r in range(len(lens)):
+        wide[r, need[r]:] = 10 ** 6  # garbage past ceil(n / B) is ignored
+    assert kvr.kv_rebuild_check(s, B, NB, toks, lens, wide) == kvr.KV_OK
+
+
+def test_zero_length_requests(L):
+    s, B, NB, toks, lens, tables = _valid(lens=(0, 3, 0))
+    assert kvr.kv_rebuild_check(s, B, NB, toks, lens, tables) == kvr.KV_OK
+    empty = kvr.kv_rebuild_check(s, B, NB, np.zeros(0, np.int32), np.zeros(0, np.int32),
+                                 np.zeros((0, 0), np.int32))
+    assert empty == kvr.KV_OK
+
+
+def test_null_pointers(L):
+    s, B, NB, toks, lens, tables = _valid()
+    d = kvr.make_desc(s)
+    i32p = C.POINTER(C.c_int32)
+    tab = np.ascontiguousarray(tables)
+    st = L.kv_rebuild_check(C.byref(d), B, NB, None, lens.ctypes.data_as(i32p), len(lens),
+                            tab.ctypes.data_as(i32p), tab.shape[1])
+    assert st == kvr.KV_EINVAL
+    st = L.kv_rebuild_check(C.byref(d), B, NB, toks.ctypes.data_as(i32p), None, len(lens),
+                            tab.ctypes.data_as(i32p), tab.shape[1])
+    assert st == kvr.KV_EINVAL
+    assert L.kv_rebuild_check(None, B, NB, None, None, 0, None, 0) == kvr.KV_EINVAL
+
+
+def test_bind_rejects_bad_arguments_before_device_access(L):
+    s = W.TINY_BF16
+    need = s.num_layers * 2 * 10 * 16 * s.num_kv_heads * s.head_dim * 2
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_arena_bind(0, need, s, 16, 10)
+    assert e.value.status == kvr.KV_EINVAL
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_arena_bind(0x10000, need - 1, s, 16, 10)  # never dereferenced: geometry fails first
+    assert e.value.status == kvr.KV_EINVAL
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_arena_bind(0x10000, need, dataclasses.replace(s, dtype=7), 16, 10)
+    assert e.value.status == kvr.KV_EINVAL
+
+
+def test_bind_forced_probe_failure(L, monkeypatch):
+    s = W.TINY_BF16
+    need = s.num_layers * 2 * 10 * 16 * s.num_kv_heads * s.head_dim * 2
+    monkeypatch.setenv("KVR_DEBUG_FAIL_PROBE", "1")
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_arena_bind(0x10000, need, s, 16, 10)
+    assert e.value.status == kvr.KV_EDEVICE
+
+
+def test_unknown_handles_are_rejected(L):
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_arena_release(0x1234)
+    assert e.value.status == kvr.KV_ESTATE
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_rebuild_stage(0x1234, [1], [1], [[0]], 0x10000, 1 << 20)
+    assert e.value.status == kvr.KV_ESTATE
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_plan_release(0x1234)
+    assert e.value.status == kvr.KV_ESTATE

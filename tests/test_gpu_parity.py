@@ -1,0 +1,261 @@
+"""GPU parity of the HIP rebuild (through the C ABI) against the CPU oracle.
+
+Tolerances: max normwise error per (layer, K|V, kv head) tensor of 1e-4 for
+fp32 models and 2e-2 for bf16 models; slot placement, untouched blocks and
+tail slots bit-exact; repeated, multi-wave and per-request rebuilds
+bit-identical to each other (deterministic kernels)."""
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from paper_2608_14635_amd import harness as Hn  # noqa: E402
+from paper_2608_14635_amd import kvr  # noqa: E402
+from paper_2608_14635_amd import workloads as W  # noqa: E402
+
+import parity_util as PU  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def gpu_rebuild(wl, model, host_image=None, wave_tokens=None, arena=None):
+    """Rebuild `wl` on the GPU; returns (arena host bits, DeviceArena)."""
+    if arena is None:
+        arena = Hn.DeviceArena(wl, host_image=host_image)
+        arena.bind()
+    T = wl.total_tokens
+    wt = wave_tokens or max(T, 1)
+    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, T, wt)
+    kvr.kv_rebuild(model.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle,
+                   ws.data_ptr(), nbytes, Hn.stream_ptr())
+    torch.cuda.synchronize()
+    return arena.to_host(), arena
+
+
+def oracle_rebuild(oracle_lib, wl, host_w, image):
+    out = image.copy()
+    oracle_lib.rebuild(wl.shape, host_w, wl.tokens, wl.lens, wl.block_tables, out, wl.block_size,
+                       wl.num_blocks)
+    return out
+
+
+def check_parity(wl, gpu_bits, ora_bits, before, tol=None):
+    worst, rep = PU.compare(wl, gpu_bits, ora_bits, before)
+    tol = tol or PU.TOL[wl.shape.dtype]
+    say(f"  {wl.name}: worst per-layer K/V error {np.array2string(worst.T, precision=2)} "
+        f"(tol {tol}); {rep}")
+    assert rep["unwritten_changed"] == 0
+    assert rep["written_nonfinite"] == 0
+    assert rep["worst"] <= tol
+
+
+# --------------------------------------------------------------------------
+def test_config1_full_fp32(oracle_lib):
+    wl = W.config1()
+    say(f"config1 fp32 lens={wl.lens.tolist()}")
+    host_w = W.host_weights(wl.shape, seed=101)
+    image = W.host_arena(wl)
+    model = Hn.device_model_from_host(wl.shape, host_w)
+    g, arena = gpu_rebuild(wl, model, host_image=image)
+    o = oracle_rebuild(oracle_lib, wl, host_w, image)
+    check_parity(wl, g, o, image)
+    arena.release()
+
+
+@pytest.fixture(scope="module")
+def tiny_bf16(oracle_lib):
+    shape = W.TINY_BF16
+    wl = W.small_workload(shape, [1, 17, 300, 129, 64, 0, 255], seed=201, other_live_frac=0.25)
+    host_w = W.host_weights(shape, seed=202)
+    image = W.host_arena(wl)
+    o = oracle_rebuild(oracle_lib, wl, host_w, image)
+    return wl, host_w, image, o
+
+
+def test_tiny_bf16_all_layers(tiny_bf16):
+    wl, host_w, image, o = tiny_bf16
+    say(f"tiny bf16 {wl.shape} lens={wl.lens.tolist()}")
+    model = Hn.device_model_from_host(wl.shape, host_w)
+    g, arena = gpu_rebuild(wl, model, host_image=image)
+    check_parity(wl, g, o, image)
+    inv = arena.check_invariants()
+    say(f"  device invariants {inv}")
+    assert inv == {"free_changed": 0, "live_changed": 0, "tail_changed": 0, "written_bad": 0}
+    arena.release()
+
+
+def test_tiny_bf16_waves_repeat_and_batch_are_bit_identical(tiny_bf16):
+    wl, host_w, image, _ = tiny_bf16
+    model = Hn.device_model_from_host(wl.shape, host_w)
+    say("tiny bf16 single wave")
+    g1, arena = gpu_rebuild(wl, model, host_image=image)
+    say("tiny bf16 repeated over garbage in the listed slots")
+    m = PU.written_mask(wl)
+    bits = arena.bits.view(arena.shape6[:4] + (-1,))
+    junk = torch.randint(-32768, 32767, bits[torch.as_tensor(m, device=bits.device)].shape,
+                         dtype=torch.int16, device=bits.device)
+    bits[torch.as_tensor(m, device=bits.device)] = junk
+    g2, _ = gpu_rebuild(wl, model, arena=arena)
+    assert np.array_equal(g1, g2), "rebuild depends on prior slot contents"
+    say("tiny bf16 in waves of <= 300 tokens")
+    arena.bits.copy_(torch.from_numpy(image.view(np.int16).copy()).view(arena.shape6).cuda())
+    g3, _ = gpu_rebuild(wl, model, arena=arena, wave_tokens=300)
+    assert np.array_equal(g1, g3), "multi-wave rebuild differs from single wave"
+    say("tiny bf16 request 2 alone")
+    off = wl.request_offsets()
+    r = 2
+    single = dataclasses.replace(wl, lens=wl.lens[r:r + 1].copy(),
+                                 tokens=wl.tokens[off[r]:off[r + 1]].copy(),
+                                 block_tables=wl.block_tables[r:r + 1].copy())
+    arena.bits.copy_(torch.from_numpy(image.view(np.int16).copy()).view(arena.shape6).cuda())
+    g4, _ = gpu_rebuild(single, model, arena=arena)
+    shp = arena.shape6
+    p = np.arange(int(wl.lens[r]))
+    blk, sl = wl.block_tables[r, p // wl.block_size], p % wl.block_size
+    a1 = g1.reshape(shp)[:, :, blk, sl]
+    a4 = g4.reshape(shp)[:, :, blk, sl]
+    assert np.array_equal(a1, a4), "request result depends on the rest of the batch"
+    arena.release()
+
+
+def test_stage_execute_matches_rebuild(tiny_bf16):
+    wl, host_w, image, o = tiny_bf16
+    model = Hn.device_model_from_host(wl.shape, host_w)
+    arena = Hn.DeviceArena(wl, host_image=image)
+    arena.bind()
+    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, wl.total_tokens, wl.total_tokens)
+    say("stage once, execute twice")
+    plan = kvr.kv_rebuild_stage(arena.handle, wl.tokens, wl.lens, wl.block_tables, ws.data_ptr(),
+                                nbytes, Hn.stream_ptr())
+    assert kvr.kv_plan_info(plan)[0] == 1
+    kvr.kv_rebuild_execute(model.weights, plan, Hn.stream_ptr())
+    torch.cuda.synchronize()
+    g1 = arena.to_host()
+    kvr.kv_rebuild_execute(model.weights, plan, Hn.stream_ptr())
+    torch.cuda.synchronize()
+    g2 = arena.to_host()
+    kvr.kv_plan_release(plan)
+    assert np.array_equal(g1, g2)
+    check_parity(wl, g1, o, image)
+    arena.release()
+
+
+def test_errors_leave_arena_untouched(tiny_bf16):
+    wl, host_w, image, _ = tiny_bf16
+    model = Hn.device_model_from_host(wl.shape, host_w)
+    arena = Hn.DeviceArena(wl, host_image=image)
+    arena.bind()
+    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, wl.total_tokens, wl.total_tokens)
+    before = arena.bits.clone()
+    cases = []
+    t = wl.tokens.copy(); t[3] = wl.shape.vocab; cases.append(("token", t, wl.lens, wl.block_tables, kvr.KV_ERANGE))
+    tb = wl.block_tables.copy(); tb[2, 1] = wl.num_blocks; cases.append(("block", wl.tokens, wl.lens, tb, kvr.KV_ERANGE))
+    tb = wl.block_tables.copy(); tb[2, 1] = tb[1, 0]; cases.append(("alias", wl.tokens, wl.lens, tb, kvr.KV_EALIAS))
+    cases.append(("capacity", wl.tokens, wl.lens, wl.block_tables[:, :2].copy(), kvr.KV_ECAPACITY))
+    for name, tok, lens, tab, expect in cases:
+        say(f"error case {name}")
+        with pytest.raises(kvr.KvError) as e:
+            kvr.kv_rebuild(model.weights, tok, lens, tab, arena.handle, ws.data_ptr(), nbytes,
+                           Hn.stream_ptr())
+        assert e.value.status == expect
+    say("error case workspace too small")
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_rebuild(model.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle,
+                       ws.data_ptr(), 4096, Hn.stream_ptr())
+    assert e.value.status == kvr.KV_ENOMEM
+    say("error case model mismatch")
+    other = Hn.device_model_from_host(wl.shape.with_layers(2), {"embed": host_w["embed"],
+                                                                "layers": host_w["layers"][:2]})
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_rebuild(other.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle,
+                       ws.data_ptr(), nbytes, Hn.stream_ptr())
+    assert e.value.status == kvr.KV_ESTATE
+    torch.cuda.synchronize()
+    assert torch.equal(before, arena.bits), "a rejected call wrote the arena"
+    arena.release()
+
+
+def test_bind_probe_and_pointer_checks():
+    wl = W.small_workload(W.TINY_BF16, [5], seed=301)
+    arena = Hn.DeviceArena(wl)
+    say("bind on device memory")
+    h = arena.bind()
+    assert h
+    arena.release()
+    say("bind on host memory is refused")
+    host = np.zeros(arena.nbytes // 2, np.int16)
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_arena_bind(host.ctypes.data, arena.nbytes, wl.shape, wl.block_size, wl.num_blocks, 0)
+    assert e.value.status == kvr.KV_EDEVICE
+
+
+# --------------------------------------------------------------------------
+# real layer widths, two layers, short requests (oracle-sized)
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("name,B", [("llama8b", 16), ("qwen14b", 32), ("qwen32b", 16)])
+def test_real_width_two_layers(oracle_lib, name, B):
+    shape = W.SHAPES[name].with_layers(2)
+    wl = W.small_workload(shape, [1, 17, 300], block_size=B, seed=401, other_live_frac=0.3)
+    say(f"{name} 2 layers B={B} lens={wl.lens.tolist()}")
+    model = Hn.device_model_random(shape, seed=402, gain_std=0.1)
+    host_w = Hn.host_copy_all(model)
+    image = W.host_arena(wl)
+    g, arena = gpu_rebuild(wl, model, host_image=image)
+    arena.release()
+    del model
+    torch.cuda.empty_cache()
+    o = oracle_rebuild(oracle_lib, wl, host_w, image)
+    check_parity(wl, g, o, image)
+
+
+# --------------------------------------------------------------------------
+# the full 8B benchmark workload: sampled layer-0 parity + invariants
+# --------------------------------------------------------------------------
+def test_full_config2_sampled_layer0_and_invariants(oracle_lib):
+    wl = W.config2()
+    say(f"config2 full: R={wl.num_requests} T={wl.total_tokens} NB={wl.num_blocks}")
+    model = Hn.device_model_random(wl.shape, seed=2)
+    arena = Hn.DeviceArena(wl)
+    arena.bind()
+    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, wl.total_tokens, wl.total_tokens)
+    kvr.kv_rebuild(model.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle,
+                   ws.data_ptr(), nbytes, Hn.stream_ptr())
+    torch.cuda.synchronize()
+    inv = arena.check_invariants()
+    say(f"  device invariants {inv}")
+    assert inv == {"free_changed": 0, "live_changed": 0, "tail_changed": 0, "written_bad": 0}
+    # sampled layer-0 K/V: first/last tokens, block boundaries, random positions
+    rng = np.random.default_rng(7)
+    off = wl.request_offsets()
+    picks = []
+    for r in range(wl.num_requests):
+        n = int(wl.lens[r])
+        cand = {0, 1, n - 1, 15, 16, 17, n // 2}
+        cand.update(rng.integers(0, n, size=24).tolist())
+        picks += [(r, p) for p in sorted(c for c in cand if 0 <= c < n)]
+    toks = np.array([wl.tokens[off[r] + p] for r, p in picks], np.int32)
+    pos = np.array([p for _, p in picks], np.int32)
+    h0 = Hn.host_copy_layer0(model)
+    k_o, v_o = oracle_lib.layer0_kv(wl.shape, h0["embed"], h0["layer0"], toks, pos)
+    B = wl.block_size
+    blk = torch.as_tensor([int(wl.block_tables[r, p // B]) for r, p in picks], device="cuda")
+    sl = torch.as_tensor([p % B for _, p in picks], device="cuda")
+    k_g = arena.bits[0, 0][blk, sl].cpu().numpy().view(np.uint16).reshape(len(picks), -1)
+    v_g = arena.bits[0, 1][blk, sl].cpu().numpy().view(np.uint16).reshape(len(picks), -1)
+    nkv, d = wl.shape.num_kv_heads, wl.shape.head_dim
+    for name, g, o in (("K", k_g, k_o), ("V", v_g, v_o)):
+        gf = W.bf16_bits_to_f32(g).reshape(-1, nkv, d).astype(np.float64)
+        of = W.bf16_bits_to_f32(o).reshape(-1, nkv, d).astype(np.float64)
+        err = max(np.max(np.abs(gf[:, h] - of[:, h])) / np.max(np.abs(of[:, h])) for h in range(nkv))
+        exact = float(np.mean(g == o))
+        say(f"  layer-0 {name} on {len(picks)} sampled slots: normwise {err:.3e}, bit-exact {exact:.3f}")
+        assert err <= PU.TOL[W.BF16]
+    arena.release()
