@@ -115,9 +115,15 @@ class DeviceArena:
         self.dt = s.dtype
         self.shape6 = (s.num_layers, 2, wl.num_blocks, wl.block_size, s.num_kv_heads, s.head_dim)
         bits_t = _TORCH_BITS[self.dt]
+        # other-live blocks of a host image keep a device copy for the checks;
+        # device-filled arenas regenerate their pattern instead
+        self.live_ref: Optional[torch.Tensor] = None
         if host_image is not None:
             arr = host_image.view(np.int16 if self.dt == W.BF16 else np.int32)
             self.bits = torch.from_numpy(arr.copy()).to(device).view(self.shape6)
+            if wl.other_live.size:
+                live = torch.as_tensor(wl.other_live, device=self.bits.device)
+                self.live_ref = self.bits[:, :, live].clone()
         else:
             self.bits = torch.empty(self.shape6, dtype=bits_t, device=device)
             self.fill_initial()
@@ -213,7 +219,9 @@ class DeviceArena:
             for kv in range(2):
                 plane = self.bits[l, kv]
                 bad["free_changed"] += int((plane[free] != sen).sum())
-                if live.numel():
+                if live.numel() and self.live_ref is not None:
+                    bad["live_changed"] += int((plane[live] != self.live_ref[l, kv]).sum())
+                elif live.numel():
                     for i in range(0, live.numel(), 4096):
                         blk = live[i:i + 4096]
                         bad["live_changed"] += int((plane[blk] != self.live_pattern(blk, 2 * l + kv)).sum())
