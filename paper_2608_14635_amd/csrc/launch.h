@@ -43,9 +43,10 @@ struct GemmParams {
   const void* A;          // [M][K] activations, K contiguous
   int64_t lda;
   int M, K;
-  const void* B0;         // weights [.][K] rows, K contiguous
+  const void* B0;         // weights [.][ldb] rows, K contiguous
   const void* B1;
   const void* B2;
+  int64_t ldb;            // B row stride in elements (0 = K)
   int bmap;
   int s0, s1;             // BMAP_QKV split points (logical columns)
   int n_begin, n_end;     // logical column range of C computed by this launch
