@@ -84,15 +84,16 @@ bool same_desc(const kv_model_desc& a, const kv_model_desc& b) {
 struct Layout {
   int64_t T = 0, W = 0, Wpad = 0, nqblk_cap = 0;
   size_t tok = 0, pos = 0, slot = 0, qblk = 0, meta_end = 0;
-  size_t rope = 0, x = 0, a = 0, q = 0, u = 0, vt = 0, hf = 0, total = 0;
+  size_t rope = 0, x = 0, a = 0, q = 0, u = 0, vt = 0, kc = 0, hf = 0, total = 0;
 };
 
+// T and W count wave rows: each request occupies round_up(len, ROW_ALIGN) rows.
 Layout make_layout(const kv_model_desc& d, int32_t R, int64_t T, int64_t W) {
   Layout L;
   L.T = T;
   L.W = W;
   L.Wpad = round_up(std::max<int64_t>(W, 1), 256);
-  L.nqblk_cap = (T + ATTN_QBLOCK - 1) / ATTN_QBLOCK + R;
+  L.nqblk_cap = (T + ATTN_QBLOCK_MIN - 1) / ATTN_QBLOCK_MIN + R;
   const int64_t e = elem_bytes(d.dtype);
   size_t off = 0;
   auto seg = [&](size_t bytes) {
@@ -111,6 +112,7 @@ Layout make_layout(const kv_model_desc& d, int32_t R, int64_t T, int64_t W) {
   L.q = seg((size_t)e * L.Wpad * d.num_q_heads * d.head_dim);
   L.u = seg((size_t)e * L.Wpad * d.num_q_heads * d.head_dim);
   L.vt = seg(d.dtype == KV_BF16 ? (size_t)2 * d.num_kv_heads * d.head_dim * L.Wpad : 0);
+  L.kc = seg(d.dtype == KV_BF16 ? (size_t)2 * d.num_kv_heads * d.head_dim * L.Wpad : 0);
   L.hf = seg((size_t)e * L.Wpad * d.ffn_dim);
   L.total = off;
   return L;
@@ -119,9 +121,11 @@ Layout make_layout(const kv_model_desc& d, int32_t R, int64_t T, int64_t W) {
 // ---------------------------------------------------------------------------
 // Handles
 // ---------------------------------------------------------------------------
+int64_t padded_rows(int64_t n) { return n > 0 ? round_up(n, ROW_ALIGN) : 0; }
+
 struct Wave {
-  int64_t tok_begin;
-  int32_t rows;
+  int64_t tok_begin;  // first metadata row of the wave
+  int32_t rows;       // rows including per-request padding (a multiple of ROW_ALIGN)
   int32_t qblk_begin, num_qblk;
   double causal_pairs;  // sum over its requests of n(n+1)/2 (query, key) pairs
 };
@@ -279,7 +283,10 @@ uint64_t kv_rebuild_workspace_bytes(const kv_model_desc* desc, int32_t num_reque
                                     int64_t total_tokens, int64_t wave_tokens) {
   if (check_desc(desc) != KV_OK || num_requests < 0 || total_tokens < 0 || wave_tokens < 0)
     return 0;
-  return make_layout(*desc, num_requests, total_tokens, std::min(wave_tokens, total_tokens)).total;
+  // every request may add up to ROW_ALIGN - 1 padding rows
+  const int64_t pad = (int64_t)(ROW_ALIGN - 1) * num_requests;
+  return make_layout(*desc, num_requests, total_tokens + pad,
+                     std::min(wave_tokens, total_tokens) + pad).total;
 }
 
 kv_status kv_rebuild_check(const kv_model_desc* desc, int32_t block_size, int64_t num_blocks,
@@ -400,34 +407,42 @@ kv_status kv_rebuild_stage(kv_arena_t arena, const int32_t* tokens, const int32_
       delete plan;
       return fail(KV_EINVAL, "null workspace");
     }
-    const Layout smallest = make_layout(d, R, T, max_len);
+    // wave rows: each request starts on a ROW_ALIGN boundary; its padding rows
+    // carry token 0, position 0 and slot -1 (computed, never scattered)
+    std::vector<int64_t> req_off(R + 1, 0), row_off(R + 1, 0);
+    for (int32_t r = 0; r < R; ++r) {
+      req_off[r + 1] = req_off[r] + lens[r];
+      row_off[r + 1] = row_off[r] + padded_rows(lens[r]);
+    }
+    const int64_t Trows = row_off[R];
+    const int64_t min_wave = padded_rows(max_len);
+    const Layout smallest = make_layout(d, R, Trows, min_wave);
     if (smallest.total > ws_bytes) {
       delete plan;
       return fail(KV_ENOMEM, "workspace of %llu bytes < %llu needed for the longest request",
                   (unsigned long long)ws_bytes, (unsigned long long)smallest.total);
     }
     // largest wave capacity whose layout fits
-    int64_t lo = max_len, hi = T;
+    int64_t lo = min_wave, hi = Trows;
     while (lo < hi) {
       const int64_t mid = lo + (hi - lo + 1) / 2;
-      if (make_layout(d, R, T, mid).total <= ws_bytes) lo = mid; else hi = mid - 1;
+      if (make_layout(d, R, Trows, mid).total <= ws_bytes) lo = mid; else hi = mid - 1;
     }
-    plan->lay = make_layout(d, R, T, lo);
+    plan->lay = make_layout(d, R, Trows, lo);
     const Layout& L = plan->lay;
 
     // waves: consecutive requests, never split
-    std::vector<int64_t> req_off(R + 1, 0);
-    for (int32_t r = 0; r < R; ++r) req_off[r + 1] = req_off[r] + lens[r];
     {
       Wave w{0, 0, 0, 0, 0.0};
       for (int32_t r = 0; r < R; ++r) {
         if (lens[r] == 0) continue;
-        if (w.rows > 0 && w.rows + (int64_t)lens[r] > L.W) {
+        const int64_t pr = padded_rows(lens[r]);
+        if (w.rows > 0 && w.rows + pr > L.W) {
           plan->waves.push_back(w);
-          w = Wave{req_off[r], 0, 0, 0, 0.0};
+          w = Wave{row_off[r], 0, 0, 0, 0.0};
         }
-        if (w.rows == 0) w.tok_begin = req_off[r];
-        w.rows += lens[r];
+        if (w.rows == 0) w.tok_begin = row_off[r];
+        w.rows += (int32_t)pr;
         w.causal_pairs += 0.5 * (double)lens[r] * ((double)lens[r] + 1.0);
       }
       if (w.rows > 0) plan->waves.push_back(w);
@@ -455,25 +470,31 @@ kv_status kv_rebuild_stage(kv_arena_t arena, const int32_t* tokens, const int32_
     int32_t* hpos = reinterpret_cast<int32_t*>(hb + L.pos);
     int64_t* hslot = reinterpret_cast<int64_t*>(hb + L.slot);
     int4* hq = reinterpret_cast<int4*>(hb + L.qblk);
-    std::memcpy(htok, tokens, sizeof(int32_t) * (size_t)T);
     const int32_t B = arena->block_size;
     for (int32_t r = 0; r < R; ++r) {
       const int32_t* tab = tables + (int64_t)r * max_blocks;
+      const int64_t r0 = row_off[r];
       for (int32_t p = 0; p < lens[r]; ++p) {
-        const int64_t t = req_off[r] + p;
-        hpos[t] = p;
-        hslot[t] = (int64_t)tab[p / B] * B + p % B;
+        htok[r0 + p] = tokens[req_off[r] + p];
+        hpos[r0 + p] = p;
+        hslot[r0 + p] = (int64_t)tab[p / B] * B + p % B;
+      }
+      for (int64_t t = r0 + lens[r]; t < row_off[r + 1]; ++t) {
+        htok[t] = 0;
+        hpos[t] = 0;
+        hslot[t] = -1;
       }
     }
+    const int QB = attn_qblock(d.dtype, d.num_q_heads / d.num_kv_heads);
     int32_t nq_total = 0;
     for (auto& w : plan->waves) {
       w.qblk_begin = nq_total;
       std::vector<int4> blocks;
       for (int32_t r = 0; r < R; ++r) {
-        if (lens[r] == 0 || req_off[r] < w.tok_begin || req_off[r] >= w.tok_begin + w.rows) continue;
-        const int32_t rs = (int32_t)(req_off[r] - w.tok_begin);
-        for (int32_t qs = 0; qs < lens[r]; qs += ATTN_QBLOCK)
-          blocks.push_back(make_int4(rs + qs, std::min(ATTN_QBLOCK, lens[r] - qs), rs, 0));
+        if (lens[r] == 0 || row_off[r] < w.tok_begin || row_off[r] >= w.tok_begin + w.rows) continue;
+        const int32_t rs = (int32_t)(row_off[r] - w.tok_begin);
+        for (int32_t qs = 0; qs < lens[r]; qs += QB)
+          blocks.push_back(make_int4(rs + qs, std::min(QB, lens[r] - qs), rs, 0));
       }
       // longest causal extent first
       std::stable_sort(blocks.begin(), blocks.end(), [](const int4& x, const int4& y) {
@@ -555,6 +576,7 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
   void* Q = ws + L.q;
   void* U = ws + L.u;
   void* VT = dt == KV_BF16 ? (void*)(ws + L.vt) : nullptr;
+  void* KC = dt == KV_BF16 ? (void*)(ws + L.kc) : nullptr;
   void* HF = ws + L.hf;
   auto gemm = dt == KV_BF16 ? launch_gemm_bf16 : launch_gemm_f32;
 
@@ -599,6 +621,7 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
       g.epi.arena_k = plane_k;
       g.epi.arena_v = plane_v;
       g.epi.vt = VT;
+      g.epi.kc = KC;
       g.epi.ldvt = L.Wpad;
       g.epi.slot = slot;
       g.epi.pos = pos;
@@ -617,6 +640,7 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
       ap.arena_k = plane_k;
       ap.arena_v = plane_v;
       ap.vt = VT;
+      ap.kc = KC;
       ap.ldvt = L.Wpad;
       ap.slot = slot;
       ap.qblk = qblk;

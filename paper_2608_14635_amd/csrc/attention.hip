@@ -1,18 +1,22 @@
 // Variable-length causal grouped-query attention of the rebuild.
 //
-// bf16 path (head_dim 128): one workgroup per (q-block of up to 128 queries of
-// one request, q head); 4 wave64s each own 32 queries.  Key tiles of 64 keys
-// are staged in LDS: K rows gathered from the arena slots through the slot
-// table (the values the decode path would read), V from the V^T copy the QKV
-// epilogue wrote.  Scores are computed transposed, S^T = K Q^T, with
-// v_mfma_f32_32x32x16_bf16: a lane then owns one query column and 32 of the 64
-// keys of the tile in registers, so the running max / sum of the online
-// softmax are per-lane scalars completed by one cross-half exchange, and the
-// probabilities P^T feed the P.V product (O^T = V^T P^T) directly from
-// registers as the B operand, without a round trip through LDS.  exp2 with
-// the scale folded in; P is rounded to bf16 for the MFMA; fp32 accumulation.
-// q-blocks are scheduled longest-first; tiles entirely above a wave's
-// diagonal are skipped.  Deterministic: fixed key order, no atomics.
+// bf16 path (head_dim 128): a workgroup is 8 wave64s = HW q heads of one GQA
+// group x QW blocks of 32 queries of one request (HW * QW = 8), so every K/V
+// tile staged in LDS feeds 8 waves.  Key tiles of 64 keys stream into a
+// 3-stage LDS ring with global_load_lds_dwordx4 (two tiles in flight): K rows
+// from a contiguous per-head copy of the stored K, V from the V^T copy, both
+// written by the QKV epilogue with the values sent to the arena.  Scores are
+// computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: a lane owns
+// one query column and 32 of the tile's keys in registers, so the online
+// softmax statistics are per-lane scalars completed by one cross-half
+// exchange, and P^T feeds O^T = V^T P^T straight from registers as the B
+// operand.  K rows are placed in LDS with bits 2 and 3 of their index swapped,
+// which makes the 8 keys of each P^T operand slot group contiguous in V^T, so
+// every V^T operand is one 16-byte LDS read.  exp2 with the scale folded in;
+// P rounded to bf16 for the MFMA; fp32 accumulation; masking only on tiles
+// that cross a wave's diagonal; the O rescale is skipped when no lane's
+// running max moved.  q-blocks are scheduled longest-first.  Deterministic:
+// fixed key order, no atomics.
 //
 // fp32 path: a plain online-softmax kernel (one wave per query, lanes across
 // head dims) for fp32 models.
@@ -23,37 +27,70 @@ namespace kvr {
 
 namespace {
 
-constexpr int QB = ATTN_QBLOCK;   // 128 queries per workgroup
-constexpr int KB = 64;            // keys per tile
 constexpr int D = 128;
-constexpr int LDKS = D + 8;       // sK row, elements (272 B)
-constexpr int LDVT = KB + 8;      // sVt row, elements (144 B)
-constexpr int NT = 256;
+constexpr int KB = 64;                       // keys per tile
+constexpr int NW = 8, NT = 64 * NW;          // 8 waves per workgroup
+constexpr int KTILE = KB * D * 2;            // 16 KB: 64 K rows of 256 B
+constexpr int VTILE = D * KB * 2;            // 16 KB: 128 V^T rows of 128 B
+constexpr int STAGE = KTILE + VTILE;
+constexpr int NSTAGE = 3;
 
-__global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
-  __shared__ __attribute__((aligned(16))) bf16_t sK[KB * LDKS];
-  __shared__ __attribute__((aligned(16))) bf16_t sVt[D * LDVT];
+typedef __attribute__((address_space(3))) void lds_void;
 
-  const int qb = blockIdx.x / p.nq, h = blockIdx.x % p.nq;
-  const int kvh = h / (p.nq / p.nkv);
+// LDS row r of a K tile holds key ksig(r): bits 2 and 3 swapped (an involution)
+__device__ __forceinline__ int ksig(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
+// K row r: 16-byte unit u at slot u ^ (r & 15); V^T row d: unit u at slot u ^ vsw(d).
+// Both make the MFMA operand reads (32 consecutive rows, one unit) conflict-free
+// for 8- or 16-lane LDS read phases.
+__device__ __forceinline__ int vsw(int d) { return (d & 7) ^ ((d >> 3) & 1); }
+
+#define KVR_WAIT_VMCNT(n) \
+  __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (((n) >> 4) << 14) | (0x7 << 4) | (0xF << 8))
+
+// Issue this wave's share (2 K blocks + 2 V^T blocks of 1 KB) of key tile
+// starting at row kbase into ring stage `stage`.
+__device__ __forceinline__ void issue_kv(char* smem, const bf16_t* Kc, const bf16_t* Vt,
+                                         int kbase, int stage, int wid, const int* k_row,
+                                         const int* k_off, const int* v_off) {
+  char* st = smem + stage * STAGE;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int qk = wid + 8 * i;
+    __builtin_amdgcn_global_load_lds(Kc + (int64_t)(kbase + k_row[i]) * D + k_off[i],
+                                     (lds_void*)(st + qk * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(Vt + kbase + v_off[i], (lds_void*)(st + KTILE + qk * 1024), 16,
+                                     0, 0);
+  }
+}
+
+template <int HW>
+__global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
+  constexpr int QW = NW / HW;
+  __shared__ __attribute__((aligned(1024))) char smem[NSTAGE * STAGE];
+
+  const int g = p.nq / p.nkv, ngrp = g / HW;
+  int bid = blockIdx.x;
+  const int qb = bid / (p.nkv * ngrp);
+  bid -= qb * p.nkv * ngrp;
+  const int kvh = bid / ngrp, hgrp = bid % ngrp;
   const int4 blk = p.qblk[qb];
   const int q_start = blk.x, q_len = blk.y, req_start = blk.z;
-  const int key_end = q_start + q_len;          // exclusive, wave-local token index
-  const int nkeys = key_end - req_start;
+  const int nkeys = q_start + q_len - req_start;
   const int ntiles = (nkeys + KB - 1) / KB;
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int qsub = wid / HW, h = kvh * g + hgrp * HW + wid % HW;
   const int half = lane >> 5, col = lane & 31;
-  const bool wave_active = wid * 32 < q_len;
-  const int qi = min(wid * 32 + col, q_len - 1);          // clamped query of this lane
-  const int qpos = q_start + qi - req_start;              // its position in the request
-  const int wave_last = min(wid * 32 + 31, q_len - 1);
-  const int wave_max_pos = q_start + wave_last - req_start;
+  const bool wave_active = qsub * 32 < q_len;
+  const int qi = min(qsub * 32 + col, q_len - 1);            // clamped query of this lane
+  const int qpos = q_start + qi - req_start;                 // its position in the request
+  const int wave_first = q_start + qsub * 32 - req_start;
+  const int wave_last = q_start + min(qsub * 32 + 31, q_len - 1) - req_start;
 
   const int ldq = p.nq * D;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(p.q);
-  const bf16_t* Kp = reinterpret_cast<const bf16_t*>(p.arena_k);
-  const bf16_t* Vt = reinterpret_cast<const bf16_t*>(p.vt);
+  const bf16_t* Kc = reinterpret_cast<const bf16_t*>(p.kc) + (int64_t)kvh * p.ldvt * D;
+  const bf16_t* Vt = reinterpret_cast<const bf16_t*>(p.vt) + (int64_t)kvh * D * p.ldvt;
 
   // Q^T fragments (B operand of S^T = K Q^T): lane holds 8 dims of its query per k-step
   bf16x8 qf[D / 16];
@@ -61,6 +98,19 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
     const bf16_t* qrow = Q + (int64_t)(q_start + qi) * ldq + h * D + half * 8;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) qf[ks] = *reinterpret_cast<const bf16x8*>(qrow + ks * 16);
+  }
+
+  // direct-to-LDS loaders: wave w issues K instructions w, w+8 (4 rows each) and
+  // V^T instructions w, w+8 (8 rows each)
+  int k_row[2], k_off[2], v_off[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int qk = wid + 8 * i;
+    const int lr = 4 * qk + (lane >> 4);                  // LDS row
+    k_row[i] = ksig(lr);                                  // key held there
+    k_off[i] = ((lane & 15) ^ (lr & 15)) * 8;             // unit fetched into this slot
+    const int dv = 8 * qk + (lane >> 3);
+    v_off[i] = dv * (int)p.ldvt + ((lane & 7) ^ vsw(dv)) * 8;
   }
 
   f32x16 acc_o[D / 32];
@@ -71,124 +121,112 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   float m_run = -INFINITY, l_run = 0.0f;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)D);
 
-  // staging of the next tile: K 4 chunks, V^T 4 chunks of 16 B per thread
-  uint4 rk[4], rv[4];
-  auto fetch = [&](int kt) {
-    const int kbase = req_start + kt * KB;
+  // fragment addressing
+  const int kslot0 = (col & 15);   // LDS row 32*k2 + col has row&15 == col&15
+  int vbase[D / 32], vsw_l[D / 32];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + NT * i;
-      const int key = c >> 4, dch = c & 15;
-      const int tok = kbase + key;
-      if (tok < key_end) {
-        const int64_t slot = p.slot[tok];
-        rk[i] = *reinterpret_cast<const uint4*>(Kp + (slot * p.nkv + kvh) * D + dch * 8);
-      } else {
-        rk[i] = make_uint4(0, 0, 0, 0);
-      }
-      const int dd = c >> 3, kc = c & 7;
-      const int t0 = kbase + kc * 8;
-      const bf16_t* src = Vt + (int64_t)(kvh * D + dd) * p.ldvt + t0;
-      if (t0 + 8 <= key_end) {
-        rv[i] = *reinterpret_cast<const uint4*>(src);
-      } else {
-        uint16_t e[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) e[j] = (t0 + j < key_end) ? src[j] : (uint16_t)0;
-        rv[i] = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
-                           e[6] | (e[7] << 16));
-      }
-    }
-  };
-  auto stash = [&]() {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + NT * i;
-      *reinterpret_cast<uint4*>(sK + (c >> 4) * LDKS + (c & 15) * 8) = rk[i];
-      *reinterpret_cast<uint4*>(sVt + (c >> 3) * LDVT + (c & 7) * 8) = rv[i];
-    }
-  };
+  for (int t = 0; t < D / 32; ++t) {
+    const int d = t * 32 + col;
+    vbase[t] = KTILE + d * 128;
+    vsw_l[t] = vsw(d);
+  }
+  // key offset (within a 32-key half) of accumulator register r: ksig(8*(r/4) + 4*half + r%4)
 
-  fetch(0);
+  issue_kv(smem, Kc, Vt, req_start, 0, wid, k_row, k_off, v_off);
+  issue_kv(smem, Kc, Vt, req_start + min(1, ntiles - 1) * KB, 1, wid, k_row, k_off, v_off);
   for (int kt = 0; kt < ntiles; ++kt) {
-    __syncthreads();  // previous tile fully consumed
-    stash();
-    __syncthreads();
-    if (kt + 1 < ntiles) fetch(kt + 1);
+    KVR_WAIT_VMCNT(4);                      // this wave's loads of tile kt have landed
+    __builtin_amdgcn_s_barrier();           // ... and every other wave's; stage of kt-1 is free
+    issue_kv(smem, Kc, Vt, req_start + min(kt + 2, ntiles - 1) * KB, (kt + 2) % NSTAGE, wid, k_row,
+             k_off, v_off);
+    const char* st = smem + (kt % NSTAGE) * STAGE;
 
-    if (wave_active && kt * KB <= wave_max_pos) {
+    if (wave_active && kt * KB <= wave_last) {
       // ---- S^T for keys [0,32) and [32,64) of the tile ----
       f32x16 s[2];
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[k2][r] = 0.0f;
-        const bf16_t* krow = sK + (k2 * 32 + col) * LDKS + half * 8;
+        const char* krow = st + (k2 * 32 + col) * 256;
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(krow + ks * 16);
+          const bf16x8 kf =
+              *reinterpret_cast<const bf16x8*>(krow + (((2 * ks + half) ^ kslot0) << 4));
           s[k2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[k2], 0, 0, 0);
         }
       }
-      // ---- mask, scale, online softmax (register r: key 8*(r/4) + 4*half + r%4) ----
+      // ---- scale, mask on diagonal tiles, online softmax ----
       float mx = m_run;
+      if (kt * KB + KB - 1 > wave_first) {
 #pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2)
+        for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kpos = kt * KB + k2 * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          const float v = kpos <= qpos ? s[k2][r] * scale_log2 : -INFINITY;
-          s[k2][r] = v;
-          mx = fmaxf(mx, v);
-        }
+          for (int r = 0; r < 16; ++r) {
+            const int kpos = kt * KB + k2 * 32 + ksig(8 * (r >> 2) + 4 * half + (r & 3));
+            const float v = kpos <= qpos ? s[k2][r] * scale_log2 : -INFINITY;
+            s[k2][r] = v;
+            mx = fmaxf(mx, v);
+          }
+      } else {
+#pragma unroll
+        for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float v = s[k2][r] * scale_log2;
+            s[k2][r] = v;
+            mx = fmaxf(mx, v);
+          }
+      }
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float alpha = exp2f(m_run - mx);
-      m_run = mx;
+      if (__any(mx > m_run)) {
+        const float alpha = exp2f(m_run - mx);
+        l_run *= alpha;
+#pragma unroll
+        for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc_o[t][r] *= alpha;
+        m_run = mx;
+      }
       float lsum = 0.0f;
       bf16x8 pf[4];
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float e = exp2f(s[k2][r] - mx);
+          const float e = exp2f(s[k2][r] - m_run);
           lsum += e;
           pf[k2 * 2 + (r >> 3)][r & 7] = (__bf16)e;
         }
-      l_run = l_run * alpha + lsum;
+      l_run += lsum;
+      // ---- O^T += V^T P^T; P^T slot j of chunk c is key 16c + 8*half + j ----
 #pragma unroll
       for (int t = 0; t < D / 32; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc_o[t][r] *= alpha;
-      // ---- O^T += V^T P^T; P^T slot j of chunk c is key 16c + 8*(j/4) + 4*half + j%4 ----
-#pragma unroll
-      for (int t = 0; t < D / 32; ++t) {
-        const bf16_t* vrow = sVt + (t * 32 + col) * LDVT + 4 * half;
-#pragma unroll
         for (int c = 0; c < 4; ++c) {
-          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow + 16 * c);
-          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16 * c + 8);
-          const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          const bf16x8 vf = *reinterpret_cast<const bf16x8*>(st + vbase[t] +
+                                                              (((2 * c + half) ^ vsw_l[t]) << 4));
           acc_o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[c], acc_o[t], 0, 0, 0);
         }
-      }
     }
   }
+  KVR_WAIT_VMCNT(0);  // trailing refetches complete before the workgroup retires
 
   if (!wave_active) return;
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;
-  const int q_local = wid * 32 + col;
+  const int q_local = qsub * 32 + col;
   if (q_local >= q_len) return;
   bf16_t* orow = reinterpret_cast<bf16_t*>(p.out) + (int64_t)(q_start + q_local) * ldq + h * D;
   // O^T register r of d-tile t: dim 32t + 8*(r/4) + 4*half + r%4
 #pragma unroll
   for (int t = 0; t < D / 32; ++t)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int dim = t * 32 + 8 * g + 4 * half;
+    for (int gq = 0; gq < 4; ++gq) {
+      const int dim = t * 32 + 8 * gq + 4 * half;
       uint2 u;
-      u.x = (uint32_t)f2bf(acc_o[t][4 * g + 0] * inv) | ((uint32_t)f2bf(acc_o[t][4 * g + 1] * inv) << 16);
-      u.y = (uint32_t)f2bf(acc_o[t][4 * g + 2] * inv) | ((uint32_t)f2bf(acc_o[t][4 * g + 3] * inv) << 16);
+      u.x = (uint32_t)f2bf(acc_o[t][4 * gq + 0] * inv) | ((uint32_t)f2bf(acc_o[t][4 * gq + 1] * inv) << 16);
+      u.y = (uint32_t)f2bf(acc_o[t][4 * gq + 2] * inv) | ((uint32_t)f2bf(acc_o[t][4 * gq + 3] * inv) << 16);
       *reinterpret_cast<uint2*>(orow + dim) = u;
     }
 }
@@ -247,7 +285,14 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
 
 void launch_attention_bf16(const AttnParams& p, hipStream_t s) {
   if (p.num_qblk <= 0) return;
-  hipLaunchKernelGGL(attn_bf16_kernel, dim3(p.num_qblk * p.nq), dim3(NT), 0, s, p);
+  const int g = p.nq / p.nkv, hw = attn_heads_per_wg(g);
+  const dim3 grid(p.num_qblk * p.nkv * (g / hw)), block(NT);
+  switch (hw) {
+    case 8: hipLaunchKernelGGL((attn_bf16_kernel<8>), grid, block, 0, s, p); break;
+    case 4: hipLaunchKernelGGL((attn_bf16_kernel<4>), grid, block, 0, s, p); break;
+    case 2: hipLaunchKernelGGL((attn_bf16_kernel<2>), grid, block, 0, s, p); break;
+    default: hipLaunchKernelGGL((attn_bf16_kernel<1>), grid, block, 0, s, p); break;
+  }
 }
 
 void launch_attention_f32(const AttnParams& p, int, hipStream_t s) {

@@ -49,7 +49,20 @@ __device__ __forceinline__ void epi_qkv(const float* sC, int ldc, int rows, int 
         dst = reinterpret_cast<T*>(e.q_out) + (int64_t)m * qcols + n0 + hh * d;
       } else {
         const int kh = (n0 - qcols) / d + hh;
-        dst = reinterpret_cast<T*>(e.arena_k) + (e.slot[m] * e.nkv + kh) * (int64_t)d;
+        const int64_t sl = e.slot[m];
+        if (e.kc != nullptr) {
+          // contiguous per-head copy for attention; padding rows hold zeros so
+          // that keys past a request's end are inert whatever their residual holds
+          T* kd = reinterpret_cast<T*>(e.kc) + ((int64_t)kh * e.ldvt + m) * d;
+          if (sl < 0) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) lo[i] = hi[i] = 0.0f;
+          }
+          store8(kd + c0, lo);
+          store8(kd + c0 + half, hi);
+        }
+        if (sl < 0) continue;  // padding row: nothing goes to the arena
+        dst = reinterpret_cast<T*>(e.arena_k) + (sl * e.nkv + kh) * (int64_t)d;
       }
       store8(dst + c0, lo);
       store8(dst + c0 + half, hi);
@@ -61,27 +74,29 @@ __device__ __forceinline__ void epi_qkv(const float* sC, int ldc, int rows, int 
       const int r = it / per_row, c0 = (it % per_row) * 8;
       const int m = m_base + r;
       if (m >= M) continue;
+      const int64_t sl = e.slot[m];
+      if (sl < 0) continue;  // padding row
       const float* src = sC + (int64_t)r * ldc + c0;
       float v[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) v[i] = src[i];
       const int col = vbase + c0;  // = kh * d + e
-      T* dst = reinterpret_cast<T*>(e.arena_v) + e.slot[m] * (int64_t)kcols + col;
+      T* dst = reinterpret_cast<T*>(e.arena_v) + sl * (int64_t)kcols + col;
       store8(dst, v);
     }
     if (e.vt != nullptr) {
-      // V^T[kh][e][m]: 8 consecutive rows of one column per item; the buffer is
-      // padded to whole tiles, so rows >= M are written (and never read).
+      // V^T[col][m]: 8 consecutive rows of one column per item; padding rows
+      // get zeros, so attention reads inert values past a request's last key
       const int rchunks = rows / 8;
       for (int it = tid; it < BN * rchunks; it += NT) {
         const int c = it % BN, rc = it / BN;
+        const int m0 = m_base + rc * 8;
+        if (m0 >= M) continue;
         const float* src = sC + (int64_t)(rc * 8) * ldc + c;
         float v[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] = src[(int64_t)i * ldc];
-        const int col = vbase + c;
-        T* dst = reinterpret_cast<T*>(e.vt) + (int64_t)col * e.ldvt + m_base + rc * 8;
-        store8(dst, v);
+        for (int i = 0; i < 8; ++i) v[i] = e.slot[m0 + i] < 0 ? 0.0f : src[(int64_t)i * ldc];
+        store8(reinterpret_cast<T*>(e.vt) + (int64_t)(vbase + c) * e.ldvt + m0, v);
       }
     }
   }

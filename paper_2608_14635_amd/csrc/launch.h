@@ -24,9 +24,10 @@ struct EpiParams {
   void* q_out;            // [rows][nq*d]
   void* arena_k;          // this layer's K plane: [slots][nkv][d]
   void* arena_v;          // this layer's V plane
-  void* vt;               // V^T [nkv][d][ldvt] (bf16 path) or null
+  void* vt;               // V^T [nkv*d][ldvt] (bf16 path) or null; row m at column m
   int64_t ldvt;
-  const int64_t* slot;    // per wave-local token: arena slot index
+  void* kc;               // K copy [nkv][ldvt][d] (bf16 path) or null; row m at row m
+  const int64_t* slot;    // per wave-local row: arena slot index, -1 for padding rows
   const int32_t* pos;     // per wave-local token: position within its request
   const float2* rope;     // [max_pos][d/2] (cos, sin)
   int nq, nkv, d;
@@ -65,21 +66,32 @@ int launch_probe(int* dev_flag, hipStream_t s);
 void launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s);
 void launch_gemm_f32(int epi, const GemmParams& p, hipStream_t s);
 
-// Attention.  qblk: per q-block int4 {q_start, q_len, req_start, 0} in wave-local
-// token indices, ordered longest-first.
+// Attention.  qblk: per q-block int4 {q_start, q_len, req_start, 0} in
+// wave-local row indices, ordered longest-first.  Each request's rows start on
+// a ROW_ALIGN boundary; the padding rows after it hold finite values.
 struct AttnParams {
   const void* q;          // [rows][nq*d]
   const void* arena_k;    // this layer's K plane
   const void* arena_v;    // this layer's V plane (fp32 path)
-  const void* vt;         // V^T [nkv][d][ldvt] (bf16 path)
+  const void* vt;         // V^T [nkv*d][ldvt] (bf16 path)
   int64_t ldvt;
+  const void* kc;         // K copy [nkv][ldvt][d] (bf16 path)
   const int64_t* slot;
   const int4* qblk;
   int num_qblk;
   void* out;              // [rows][nq*d]
   int nq, nkv, d;
 };
-constexpr int ATTN_QBLOCK = 128;  // queries per q-block (bf16 path)
+// bf16 attention workgroups are 8 waves: HW heads of one GQA group x QW blocks
+// of 32 queries (HW = largest of 8/4/2/1 dividing the group size).
+inline int attn_heads_per_wg(int group) {
+  return group % 8 == 0 ? 8 : group % 4 == 0 ? 4 : group % 2 == 0 ? 2 : 1;
+}
+inline int attn_qblock(int dtype, int group) {
+  return dtype == 1 ? 32 * (8 / attn_heads_per_wg(group)) : 128;
+}
+constexpr int ATTN_QBLOCK_MIN = 32;
+constexpr int ROW_ALIGN = 64;  // each request's rows start on this boundary of the wave
 void launch_attention_bf16(const AttnParams& p, hipStream_t s);
 void launch_attention_f32(const AttnParams& p, int rows_total, hipStream_t s);
 

@@ -26,6 +26,30 @@ def say(msg):
     sys.stdout.flush()
 
 
+def describe_diff(wl, a, b):
+    """Where two arena images differ: per (layer, plane, request) counts."""
+    s = wl.shape
+    shp = (s.num_layers, 2, wl.num_blocks, wl.block_size, s.num_kv_heads * s.head_dim)
+    va, vb = a.reshape(shp), b.reshape(shp)
+    out = []
+    for r in range(wl.num_requests):
+        n = int(wl.lens[r])
+        if n == 0:
+            continue
+        p = np.arange(n)
+        blk, sl = wl.block_tables[r, p // wl.block_size], p % wl.block_size
+        for l in range(s.num_layers):
+            for kv in range(2):
+                x, y = va[l, kv, blk, sl], vb[l, kv, blk, sl]
+                bad = np.nonzero(np.any(x != y, axis=1))[0]
+                if bad.size:
+                    fx = W.bf16_bits_to_f32(x).astype(np.float64) if s.dtype == W.BF16 else x.view(np.float32)
+                    fy = W.bf16_bits_to_f32(y).astype(np.float64) if s.dtype == W.BF16 else y.view(np.float32)
+                    out.append(f"req {r} (n={n}) layer {l} {'KV'[kv]}: {bad.size} positions differ, "
+                               f"first {bad[:6].tolist()}, max |diff| {np.max(np.abs(fx - fy)):.3e}")
+    return out
+
+
 def gpu_rebuild(wl, model, host_image=None, wave_tokens=None, arena=None):
     """Rebuild `wl` on the GPU; returns (arena host bits, DeviceArena)."""
     if arena is None:
@@ -108,6 +132,9 @@ def test_tiny_bf16_waves_repeat_and_batch_are_bit_identical(tiny_bf16):
     say("tiny bf16 in waves of <= 300 tokens")
     arena.bits.copy_(torch.from_numpy(image.view(np.int16).copy()).view(arena.shape6).cuda())
     g3, _ = gpu_rebuild(wl, model, arena=arena, wave_tokens=300)
+    if not np.array_equal(g1, g3):
+        for line in describe_diff(wl, g1, g3)[:40]:
+            say("  " + line)
     assert np.array_equal(g1, g3), "multi-wave rebuild differs from single wave"
     say("tiny bf16 request 2 alone")
     off = wl.request_offsets()
