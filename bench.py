@@ -28,6 +28,38 @@ PEAK_BF16_TFLOPS = 2517.0   # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 fl
 PEAK_FP32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 
+# kernel class -> sources whose text fixes that kernel's code
+KERNEL_SOURCES = {
+    "gemm_qkv": ["gemm_bf16.hip", "epilogue.h", "common.h", "launch.h"],
+    "gemm_o": ["gemm_bf16.hip", "epilogue.h", "common.h", "launch.h"],
+    "gemm_gateup": ["gemm_bf16.hip", "epilogue.h", "common.h", "launch.h"],
+    "gemm_down": ["gemm_bf16.hip", "epilogue.h", "common.h", "launch.h"],
+    "attention": ["attention.hip", "common.h", "launch.h"],
+}
+
+
+def kernel_source_hash(kernel: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES.get(kernel, []):
+        with open(os.path.join(ROOT, "paper_2608_14635_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter runs (profiles/traffic.json),
+    or None when they were taken on other kernel sources or another workload."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f).get(kernel)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_sha") != kernel_source_hash(kernel) or rec.get("workload") != workload:
+        return None
+    return rec.get("bytes_per_launch")
+
 
 def algorithmic_work(wl):
     """Flops and HBM bytes the method must spend (last layer: K/V projections only)."""
@@ -103,7 +135,19 @@ def main():
     ap.add_argument("--wave-tokens", type=int, default=0, help="0 = largest that fits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0,
+                    help="only copy this many bytes device-to-device (counter calibration)")
     args = ap.parse_args()
+    if args.copy_probe:
+        import torch
+        n = args.copy_probe // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n * 4}))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
@@ -213,7 +257,12 @@ def main():
                    "ffn": shape.ffn_dim, "vocab": shape.vocab, "waves": n_waves,
                    "max_wave_tokens": max_wave, "weights": "random N(0,0.02)"},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": dom_tf, "peak": peak,
-                     "unit": "TFLOP/s", "frac": dom_tf / peak, "traffic": None},
+                     "unit": "TFLOP/s", "frac": dom_tf / peak,
+                     "traffic": measured_traffic(dom, wl.name),
+                     "launches": prof[dom]["launches"],
+                     "avg_launch_ms": prof[dom]["ms"] / max(1, prof[dom]["launches"]),
+                     "flop_per_launch": prof[dom]["flops"] / max(1, prof[dom]["launches"]),
+                     "source_sha": kernel_source_hash(dom)},
         "end_to_end": {"algorithmic_tflop": work["flops"] / 1e12,
                        "mfma_frac": work["flops"] / sec / 1e12 / peak,
                        "hbm_frac": work["bytes"] / sec / 1e9 / PEAK_HBM_GBS,

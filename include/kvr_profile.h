@@ -5,7 +5,8 @@
  * two HIP events on the caller's stream.  kv_profile_read waits for the
  * recorded events and returns, per kernel class, the accumulated device time
  * (ms), the number of launches and the algorithmic flops of those launches
- * (GEMMs: 2*M*N*K; attention: 4*nq*d per visible causal (query, key) pair).
+ * (GEMMs: 2*T*N*K over the real, unpadded tokens T; attention: 4*nq*d per
+ * visible causal (query, key) pair).
  * Used for roofline accounting; adds two event records per launch.
  */
 #ifndef KVR_PROFILE_H

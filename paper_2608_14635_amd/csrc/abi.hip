@@ -128,6 +128,7 @@ struct Wave {
   int32_t rows;       // rows including per-request padding (a multiple of ROW_ALIGN)
   int32_t qblk_begin, num_qblk;
   double causal_pairs;  // sum over its requests of n(n+1)/2 (query, key) pairs
+  int64_t tokens;       // real (unpadded) tokens
 };
 
 }  // namespace
@@ -433,17 +434,18 @@ kv_status kv_rebuild_stage(kv_arena_t arena, const int32_t* tokens, const int32_
 
     // waves: consecutive requests, never split
     {
-      Wave w{0, 0, 0, 0, 0.0};
+      Wave w{0, 0, 0, 0, 0.0, 0};
       for (int32_t r = 0; r < R; ++r) {
         if (lens[r] == 0) continue;
         const int64_t pr = padded_rows(lens[r]);
         if (w.rows > 0 && w.rows + pr > L.W) {
           plan->waves.push_back(w);
-          w = Wave{row_off[r], 0, 0, 0, 0.0};
+          w = Wave{row_off[r], 0, 0, 0, 0.0, 0};
         }
         if (w.rows == 0) w.tok_begin = row_off[r];
         w.rows += (int32_t)pr;
         w.causal_pairs += 0.5 * (double)lens[r] * ((double)lens[r] + 1.0);
+        w.tokens += lens[r];
       }
       if (w.rows > 0) plan->waves.push_back(w);
     }
@@ -630,7 +632,7 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
       g.epi.nkv = nkv;
       g.epi.d = hd;
       {
-        ProfScope ps(ar, s, KV_PROF_GEMM_QKV, 2.0 * M * (double)(g.n_end - g.n_begin) * H);
+        ProfScope ps(ar, s, KV_PROF_GEMM_QKV, 2.0 * wv.tokens * (double)(g.n_end - g.n_begin) * H);
         gemm(EPI_QKV, g, s);
       }
       if (last) break;
@@ -667,7 +669,7 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
       go.epi.x = X;
       go.epi.ldx = H;
       {
-        ProfScope ps(ar, s, KV_PROF_GEMM_O, 2.0 * M * (double)H * nq * hd);
+        ProfScope ps(ar, s, KV_PROF_GEMM_O, 2.0 * wv.tokens * (double)H * nq * hd);
         gemm(EPI_RESID, go, s);
       }
       {
@@ -688,7 +690,7 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
       gu.epi.ldh = F;
       gu.epi.ffn = F;
       {
-        ProfScope ps(ar, s, KV_PROF_GEMM_GATEUP, 2.0 * M * 2.0 * F * H);
+        ProfScope ps(ar, s, KV_PROF_GEMM_GATEUP, 2.0 * wv.tokens * 2.0 * F * H);
         gemm(EPI_SWIGLU, gu, s);
       }
       GemmParams gd{};
@@ -703,7 +705,7 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
       gd.epi.x = X;
       gd.epi.ldx = H;
       {
-        ProfScope ps(ar, s, KV_PROF_GEMM_DOWN, 2.0 * M * (double)H * F);
+        ProfScope ps(ar, s, KV_PROF_GEMM_DOWN, 2.0 * wv.tokens * (double)H * F);
         gemm(EPI_RESID, gd, s);
       }
     }
