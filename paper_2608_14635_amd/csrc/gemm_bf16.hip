@@ -1,16 +1,16 @@
 // bf16 GEMM C[M, N] = A[M, K] . B[N, K]^T on gfx950 matrix cores, with the
 // rebuild's epilogues fused (RoPE + K/V scatter, residual add, SwiGLU).
 //
-// Tile 256 x 256 x 32, 256 threads = 4 wave64s in a 2 x 2 layout, each wave
-// owning 128 x 128 outputs as 4 x 4 v_mfma_f32_32x32x16_bf16 tiles (256 fp32
-// accumulators per lane).  Both operands are K-contiguous, so every MFMA
-// operand is one 16-byte LDS read.  Operand tiles stream from global memory
-// straight into a 4-stage LDS ring with global_load_lds_dwordx4 (no register
-// staging), keeping three K tiles (96 KB) in flight per CU to cover memory
-// latency; one barrier per K tile.  Workgroups are remapped
-// so that each XCD (dispatch round-robins workgroups over the 8 XCDs) works
-// on a contiguous range of tiles, walked in groups of 8 M-tiles so that the
-// 32 CUs of an XCD share A rows and B columns in their L2.
+// Tile 256 x 256 x 64 per workgroup of WAVES wave64s (4: a 2 x 2 layout of
+// 128 x 128 wave tiles; 8: a 2 x 4 layout of 128 x 64 wave tiles, two waves
+// per SIMD), each wave tile made of 32 x 32 v_mfma_f32_32x32x16_bf16 tiles.
+// Both operands are K-contiguous, so every MFMA operand is one 16-byte LDS
+// read.  Operand tiles stream from global memory straight into a 5-slot LDS
+// ring with buffer_load_dwordx4 ... lds (no register staging), three slots
+// (96 KB) in flight per CU.  Workgroups are remapped so that each XCD
+// (dispatch round-robins workgroups over the 8 XCDs) works on a contiguous
+// range of tiles, walked in groups of GROUP_M M-tiles so that the 32 CUs of
+// an XCD share A rows and B columns in their L2.
 // Every output element is produced by exactly one workgroup with a fixed K
 // order: results are deterministic run to run.
 #include "common.h"
@@ -21,31 +21,46 @@ namespace kvr {
 
 namespace {
 
-constexpr int BM = 256, BN = 256;
-constexpr int NT = 256;
-constexpr int LDC = BN + 4;  // epilogue fp32 tile row, elements
-constexpr int EPI_BYTES = 128 * LDC * 4;
-constexpr int GROUP_M = 8;
+#ifndef KVR_GEMM_WAVES
+#define KVR_GEMM_WAVES 4
+#endif
+#ifndef KVR_GEMM_GROUP_M
+#define KVR_GEMM_GROUP_M 8
+#endif
 
-// LDS layout of one 256-row x BK operand tile: 1 KB blocks of RPB rows of
-// BK*2 bytes; in a block, row j holds its 16-byte k-units u at slot
+constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int WAVES = KVR_GEMM_WAVES;
+constexpr int NT = 64 * WAVES;
+constexpr int WN = WAVES / 2;        // waves along N (2 along M)
+constexpr int FI = 4;                // 32-row MFMA tiles per wave (128 rows)
+constexpr int FJ = (BN / WN) / 32;   // 32-column MFMA tiles per wave
+constexpr int LDC = BN + 4;          // epilogue fp32 tile row, elements
+constexpr int EPI_BYTES = 128 * LDC * 4;
+constexpr int GROUP_M = KVR_GEMM_GROUP_M;
+static_assert(WAVES == 4 || WAVES == 8, "2 x 2 or 2 x 4 wave layout");
+
+// LDS layout of one 256-row x 64-k operand tile: 1 KB blocks of 8 rows of
+// 128 bytes; in a block, row j holds its 16-byte k-units u at slot
 // u ^ swz(j, block).  A direct-to-LDS load writes 64 lanes x 16 B
-// contiguously, so one instruction fills one block with UPR lanes per row
-// (each row's bytes are one coalesced segment).  The swizzle makes the MFMA
-// operand reads (32 consecutive rows, one k-unit) conflict-free whether the
-// LDS serves 8 or 16 lanes of a b128 read per pass.
-template <int BK> struct Ring {
-  static constexpr int UPR = BK / 8;                       // 16-byte units per row
-  static constexpr int RPB = 1024 / (BK * 2);              // rows per 1 KB block
-  static constexpr int BLOCKS = BM / RPB;                  // blocks per operand tile
-  static constexpr int HALF = BM * BK * 2;                 // bytes per operand tile
-  static constexpr int STAGE = 2 * HALF;
-  static constexpr int NSTAGE = BK == 32 ? 4 : 2;          // 128 KB ring either way
-  static constexpr int BYTES = NSTAGE * STAGE;
-  static constexpr int LOADS = BLOCKS / 4;                 // per wave, per operand, per stage
-  static __device__ __forceinline__ int swz(int j, int blk) {
-    return BK == 32 ? (((j >> 1) ^ (j >> 3)) & 3) : ((j ^ (blk & 1)) & 7);
-  }
+// contiguously, so one instruction fills one block with 8 lanes per row
+// (each row's 128 bytes are one coalesced segment: one full L2 line per
+// request, which moves twice the bytes per request of 64-byte rows).  The
+// swizzle makes the MFMA operand reads (32 consecutive rows, one k-unit)
+// conflict-free whether the LDS serves 8 or 16 lanes of a b128 read per pass.
+//
+// The ring holds NSLOT operand tiles.  Slot sequence number s carries the A
+// tile (s even) or the B tile (s odd) of K tile s/2 and lives at ring position
+// s % NSLOT.  While K tile kt is multiplied, its two slots are read and the
+// loads of the next NSLOT-2 slots are in flight.
+struct Ring {
+  static constexpr int UPR = BK / 8;           // 16-byte units per row
+  static constexpr int RPB = 1024 / (BK * 2);  // rows per 1 KB block
+  static constexpr int BLOCKS = BM / RPB;      // blocks per operand tile
+  static constexpr int HALF = BM * BK * 2;     // bytes per operand tile
+  static constexpr int NSLOT = 5;              // 160 KB
+  static constexpr int BYTES = NSLOT * HALF;
+  static constexpr int LOADS = BLOCKS / WAVES; // per wave, per slot
+  static __device__ __forceinline__ int swz(int j, int blk) { return (j ^ (blk & 1)) & 7; }
 };
 
 __device__ __forceinline__ const bf16_t* b_row_ptr(const GemmParams& p, int tile_n, int r) {
@@ -66,32 +81,81 @@ __device__ __forceinline__ const bf16_t* b_row_ptr(const GemmParams& p, int tile
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Issue the direct-to-LDS loads of K tile kt (wave `wid` fills blocks wid, wid+4, ...)
-// K tile `kt` goes to the ring stage of tile `slot_kt` (they differ only for the
-// refetches past the last tile).
-template <int BK, int Q0 = 0, int Q1 = Ring<BK>::LOADS>
-__device__ __forceinline__ void issue_tile(char* smem, const bf16_t* const* a_src,
-                                           const bf16_t* const* b_src, int kt, int slot_kt,
-                                           int wid) {
-  using R = Ring<BK>;
-  const int k0 = kt * BK;
-  char* st = smem + (slot_kt % R::NSTAGE) * R::STAGE;
+// Operand sources of one workgroup as buffer resources.  Buffer loads with
+// the LDS bit (buffer_load_dwordx4 ... lds) are tracked by the vector-memory
+// counter alone, so the LDS reads of the fragments keep exact lgkm counts;
+// the global_load_lds form would also be counted as an LDS access and force a
+// full lgkmcnt(0) drain before every k-step.
+//   A: one resource at the tile's first row; each load q has its own lane
+//      offset (rows past M are clamped to row M-1, their results dropped).
+//   B: rows 0..127 and 128..255 of the tile each sit in one weight matrix
+//      (the QKV split points are multiples of 256 and a gate/up tile is 128
+//      gate rows then 128 up rows); the block's row offset is scalar.
+struct Loader {
+  const void* a;            // tile row 0 of A
+  const void* b_lo;         // tile row 0 of B
+  const void* b_hi;         // tile row 128 of B
+  int a_bytes, b_bytes;     // extents of the three resources
+  int a_voff[Ring::LOADS];
+  int b_voff;
+  int b_block_bytes;        // bytes between consecutive 8-row blocks of B
+};
+
+constexpr int BUF_WORD3 = 0x00020000;  // gfx9 buffer descriptor: 32-bit data format
+
+// Issue loads q in [Q0, Q1) of one ring slot holding operand B (IS_B) or A at
+// K tile kt, into ring position slot % NSLOT (wave `wid` fills blocks wid,
+// wid+WAVES, ...).
+template <bool IS_B, int Q0, int Q1>
+__device__ __forceinline__ void issue_slot(char* smem, const Loader& L, int kt, int slot, int wid) {
+  const int kbytes = kt * BK * 2;
+  char* st = smem + (slot % Ring::NSLOT) * Ring::HALF;
 #pragma unroll
   for (int q = Q0; q < Q1; ++q) {
-    __builtin_amdgcn_global_load_lds(a_src[q] + k0, (lds_void*)(st + (wid + 4 * q) * 1024), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(b_src[q] + k0, (lds_void*)(st + R::HALF + (wid + 4 * q) * 1024),
-                                     16, 0, 0);
+    lds_void* dst = (lds_void*)(st + (wid + WAVES * q) * 1024);
+    if constexpr (IS_B) {
+      constexpr int HB = Ring::BLOCKS / 2;  // blocks per 128-row half
+      const bool hi = q >= Ring::LOADS / 2;
+      const int soff = kbytes + (wid + WAVES * q - (hi ? HB : 0)) * L.b_block_bytes;
+      const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(hi ? L.b_hi : L.b_lo), 0,
+                                                          L.b_bytes, BUF_WORD3);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, L.b_voff, soff, 0, 0);
+    } else {
+      const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(L.a), 0, L.a_bytes,
+                                                          BUF_WORD3);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, L.a_voff[q], kbytes, 0, 0);
+    }
   }
+}
+
+template <bool IS_B>
+__device__ __forceinline__ void issue_whole(char* smem, const Loader& L, int kt, int slot, int wid) {
+  issue_slot<IS_B, 0, Ring::LOADS>(smem, L, kt, slot, wid);
+}
+
+// Share of k-step KS in the load issue of a K tile's two slots s0 and s0+1:
+// the first half of the k-steps issues slot s0, the second half slot s0+1.
+template <int KS, bool S0_IS_B>
+__device__ __forceinline__ void issue_step(char* smem, const Loader& L, int k_s0, int k_s1, int s0,
+                                           int wid) {
+  constexpr int SPS = (BK / 16) / 2;  // k-steps per slot
+  constexpr int QS = Ring::LOADS / SPS;
+  if constexpr (KS < SPS)
+    issue_slot<S0_IS_B, (KS % SPS) * QS, (KS % SPS + 1) * QS>(smem, L, k_s0, s0, wid);
+  else
+    issue_slot<!S0_IS_B, (KS % SPS) * QS, (KS % SPS + 1) * QS>(smem, L, k_s1, s0 + 1, wid);
 }
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding)
 #define KVR_WAIT_VMCNT(n) \
   __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (((n) >> 4) << 14) | (0x7 << 4) | (0xF << 8))
 
-template <int EPI, int BK>
+// sched_group_barrier masks
+constexpr int SG_MFMA = 0x008, SG_VMEM = 0x010, SG_DS_READ = 0x100;
+
+template <int EPI>
 __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m, int tiles_n) {
-  using R = Ring<BK>;
-  constexpr int SMEM = R::BYTES > EPI_BYTES ? R::BYTES : EPI_BYTES;
+  constexpr int SMEM = Ring::BYTES > EPI_BYTES ? Ring::BYTES : EPI_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   // ---- tile coordinates: XCD-contiguous ranges, grouped along M ----
@@ -105,114 +169,184 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
   const int tile_m = first_m + (t % (GROUP_M * tiles_n)) % gsz;
   const int tile_n = (t % (GROUP_M * tiles_n)) / gsz;
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int wm = wave / WN, wn = wave % WN;
   const int m0 = tile_m * BM;
 
-  // ---- direct-to-LDS loaders: wave w fills blocks w, w+4, ... of A and of B ----
-  const int lrow = lane / R::UPR;  // row within the block
-  const bf16_t* A = reinterpret_cast<const bf16_t*>(p.A);
-  const bf16_t* a_src[R::LOADS];
-  const bf16_t* b_src[R::LOADS];
+  // ---- direct-to-LDS loaders: wave w fills blocks w, w+WAVES, ... of A and of B ----
+  const int lrow = lane / Ring::UPR;  // row within the block
+  // k-unit that lands in this lane's 16-byte slot (swz depends on the block
+  // only through its parity, which is the wave's parity for every load)
+  const int unit = (lane % Ring::UPR) ^ Ring::swz(lrow, wave);
+  Loader L;
+  {
+    const int64_t ldb = p.ldb ? p.ldb : p.K;
+    const int rows_a = min(BM, p.M - m0);
+    L.a = reinterpret_cast<const bf16_t*>(p.A) + (int64_t)m0 * p.lda;
+    L.a_bytes = (int)(rows_a * p.lda * 2);
 #pragma unroll
-  for (int q = 0; q < R::LOADS; ++q) {
-    const int blk = wid + 4 * q;
-    const int r = blk * R::RPB + lrow;
-    const int unit = (lane % R::UPR) ^ R::swz(lrow, blk);  // k-unit landing in this lane's slot
-    // rows past M read a valid row; their results are dropped by the epilogue
-    a_src[q] = A + (int64_t)min(m0 + r, p.M - 1) * p.lda + unit * 8;
-    b_src[q] = b_row_ptr(p, tile_n, r) + unit * 8;
+    for (int q = 0; q < Ring::LOADS; ++q) {
+      const int r = min((wave + WAVES * q) * Ring::RPB + lrow, rows_a - 1);
+      L.a_voff[q] = (int)(r * p.lda * 2) + unit * 16;
+    }
+    L.b_bytes = (int)((BN / 2) * ldb * 2);
+    L.b_lo = b_row_ptr(p, tile_n, 0);
+    L.b_hi = b_row_ptr(p, tile_n, BN / 2);
+    L.b_voff = (int)(lrow * ldb * 2) + unit * 16;
+    L.b_block_bytes = (int)(Ring::RPB * ldb * 2);
   }
 
-  f32x16 acc[4][4];
+  f32x16 acc[FI][FJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < FI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < FJ; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int KT = p.K / BK;
 #pragma unroll
-  for (int s = 0; s < R::NSTAGE - 1; ++s)
-    issue_tile<BK>(smem, a_src, b_src, min(s, KT - 1), s, wid);
+  for (int s = 0; s < Ring::NSLOT - 2; ++s) {
+    if (s & 1)
+      issue_whole<true>(smem, L, min(s >> 1, KT - 1), s, wave);
+    else
+      issue_whole<false>(smem, L, min(s >> 1, KT - 1), s, wave);
+  }
 
   // fragment reads: lane%32 picks the row, lane/32 the 8-wide k half
   const int fr = lane & 31, fhalf = lane >> 5;
-  const int fj = fr % R::RPB;
-  int a_base[4], b_base[4], a_sw[4], b_sw[4];
+  const int fj = fr % Ring::RPB;
+  int a_base[FI], b_base[FJ], a_sw[FI], b_sw[FJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int ra = wm * 128 + i * 32 + fr, rb = wn * 128 + i * 32 + fr;
-    a_base[i] = (ra / R::RPB) * 1024 + fj * BK * 2;
-    b_base[i] = R::HALF + (rb / R::RPB) * 1024 + fj * BK * 2;
-    a_sw[i] = R::swz(fj, ra / R::RPB);
-    b_sw[i] = R::swz(fj, rb / R::RPB);
+  for (int i = 0; i < FI; ++i) {
+    const int ra = wm * 128 + i * 32 + fr;
+    a_base[i] = (ra / Ring::RPB) * 1024 + fj * BK * 2;
+    a_sw[i] = Ring::swz(fj, ra / Ring::RPB);
+  }
+#pragma unroll
+  for (int j = 0; j < FJ; ++j) {
+    const int rb = wn * (BN / WN) + j * 32 + fr;
+    b_base[j] = (rb / Ring::RPB) * 1024 + fj * BK * 2;
+    b_sw[j] = Ring::swz(fj, rb / Ring::RPB);
   }
 
-  constexpr int PER_TILE = 2 * R::LOADS;  // load instructions per wave per K tile
+  // Slots issued during K tile kt: s0 (the operand of parity NSLOT) and s1.
+  // NSLOT-2 slots are always in flight (past the end, the last K tile is
+  // fetched again into a position no later K tile reads), so both slots of a
+  // K tile have landed once at most NSLOT-4 slots' loads are pending.
+  constexpr bool S0_IS_B = (Ring::NSLOT & 1) != 0;
+  constexpr int KS = BK / 16;                    // k-steps per K tile
+  constexpr int MF = FI * FJ;                    // MFMAs per k-step
+  constexpr int NRD = FI + FJ;                   // fragment reads per k-step
+  constexpr int NLOAD = 2 * Ring::LOADS / KS;    // buffer loads per k-step
+  constexpr int NRD2 = (NRD + 1) / 2;            // MFMAs carrying the next K tile's reads
+  // MFMAs of the last k-step issued before its barrier
+  constexpr int PBAR = MF - (NRD2 > MF / 4 ? NRD2 : MF / 4);
+  static_assert(KS % 2 == 0 && NLOAD <= PBAR && NRD2 <= MF - PBAR && NRD + NLOAD <= MF,
+                "k-step schedule");
+  constexpr int LANDED = (Ring::NSLOT - 4) * Ring::LOADS;
+
+  // K tile 0 lands; every wave sees every wave's loads after the barrier (a
+  // bare s_barrier: __syncthreads() would also drain the loads in flight).
+  KVR_WAIT_VMCNT(LANDED);
+  __builtin_amdgcn_s_barrier();
+  bf16x8 af[2][FI], bfr[2][FJ];
+#pragma unroll
+  for (int i = 0; i < FI; ++i)
+    af[0][i] = *reinterpret_cast<const bf16x8*>(smem + a_base[i] + ((fhalf ^ a_sw[i]) << 4));
+#pragma unroll
+  for (int j = 0; j < FJ; ++j)
+    bfr[0][j] = *reinterpret_cast<const bf16x8*>(smem + Ring::HALF + b_base[j] + ((fhalf ^ b_sw[j]) << 4));
+  __builtin_amdgcn_sched_barrier(0);
+
   for (int kt = 0; kt < KT; ++kt) {
-    // NSTAGE-1 tiles are always in flight (past the end, the last tile is
-    // fetched again into a stage no later iteration reads), so tile kt has
-    // landed once at most NSTAGE-2 tiles' loads are pending.
-    KVR_WAIT_VMCNT((R::NSTAGE - 2) * PER_TILE);
-    // every wave's loads of tile kt are in LDS and every wave is done reading the
-    // stage of tile kt-1.  A bare s_barrier: __syncthreads() would also drain
-    // the loads still in flight for the next tiles.
-    __builtin_amdgcn_s_barrier();
-    const int kn = min(kt + R::NSTAGE - 1, KT - 1), sn = kt + R::NSTAGE - 1;
-    const char* st = smem + (kt % R::NSTAGE) * R::STAGE;
-    // Fragments of k-step ks+1 are read from LDS while the MFMAs of k-step ks
-    // run: the A fragments before its first MFMA, the B fragments after its
-    // eighth, so that at most 12 LDS reads are ever pending (the lgkm counter
-    // tops out at 15).  sched_barrier fences keep the compiler from sinking
-    // the reads back next to their uses.
-    bf16x8 af[2][4], bfr[2][4];
+    const int s0 = 2 * kt + Ring::NSLOT - 2;
+    const int k_s0 = min(s0 >> 1, KT - 1), k_s1 = min((s0 + 1) >> 1, KT - 1);
+    const char* sta = smem + ((2 * kt) % Ring::NSLOT) * Ring::HALF;
+    const char* stb = smem + ((2 * kt + 1) % Ring::NSLOT) * Ring::HALF;
+    const char* sta_n = smem + ((2 * kt + 2) % Ring::NSLOT) * Ring::HALF;
+    const char* stb_n = smem + ((2 * kt + 3) % Ring::NSLOT) * Ring::HALF;
+    // The fragments of k-step ks+1 are read from LDS while the MFMAs of k-step
+    // ks run, and the instruction stream interleaves them one by one with the
+    // MFMAs (an MFMA keeps the pipe busy for 32 cycles while the next
+    // instruction issues): (MFMA, LDS read) pairs, then (MFMA, buffer load)
+    // pairs for the k-step's share of the next slots' loads.  The barrier that
+    // hands K tile kt+1 over sits inside the last k-step of K tile kt, after
+    // PBAR of its MFMAs: by then every fragment of K tile kt is in registers,
+    // so the slots of K tile kt may be refilled, and the first fragments of
+    // K tile kt+1 are read behind the remaining MFMAs instead of stalling the
+    // start of the next K tile.
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      af[0][i] = *reinterpret_cast<const bf16x8*>(st + a_base[i] + ((fhalf ^ a_sw[i]) << 4));
-      bfr[0][i] = *reinterpret_cast<const bf16x8*>(st + b_base[i] + ((fhalf ^ b_sw[i]) << 4));
-    }
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
+    for (int ks = 0; ks < KS; ++ks) {
       const int cur = ks & 1;
-      const int cn = 2 * (ks + 1) + fhalf;
-      if (ks + 1 < BK / 16) {
+      if (ks + 1 < KS) {
+        // in the order the next k-step's MFMAs consume them: A0, B0..B3, A1..
+        const int cn = 2 * (ks + 1) + fhalf;
+        af[cur ^ 1][0] = *reinterpret_cast<const bf16x8*>(sta + a_base[0] + ((cn ^ a_sw[0]) << 4));
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          af[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(st + a_base[i] + ((cn ^ a_sw[i]) << 4));
+        for (int j = 0; j < FJ; ++j)
+          bfr[cur ^ 1][j] = *reinterpret_cast<const bf16x8*>(stb + b_base[j] + ((cn ^ b_sw[j]) << 4));
+#pragma unroll
+        for (int i = 1; i < FI; ++i)
+          af[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(sta + a_base[i] + ((cn ^ a_sw[i]) << 4));
       }
-      // spread the next tile's load issue over this tile's k-steps
-      constexpr int QS = R::LOADS / (BK / 16);
-      if (ks == 0) issue_tile<BK, 0 * QS, 1 * QS>(smem, a_src, b_src, kn, sn, wid);
-      if (ks == 1) issue_tile<BK, 1 * QS, 2 * QS>(smem, a_src, b_src, kn, sn, wid);
-      if (ks == 2) issue_tile<BK, 2 * QS, 3 * QS>(smem, a_src, b_src, kn, sn, wid);
-      if (ks == 3) issue_tile<BK, 3 * QS, 4 * QS>(smem, a_src, b_src, kn, sn, wid);
-      __builtin_amdgcn_sched_barrier(0);
+      if (ks == 0) issue_step<0, S0_IS_B>(smem, L, k_s0, k_s1, s0, wave);
+      if (ks == 1) issue_step<1, S0_IS_B>(smem, L, k_s0, k_s1, s0, wave);
+      if (ks == 2) issue_step<2, S0_IS_B>(smem, L, k_s0, k_s1, s0, wave);
+      if (ks == 3) issue_step<3, S0_IS_B>(smem, L, k_s0, k_s1, s0, wave);
+      const int m_end = ks + 1 < KS ? MF : PBAR;
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int m = 0; m < m_end; ++m)
+        acc[m / FJ][m % FJ] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            af[cur][m / FJ], bfr[cur][m % FJ], acc[m / FJ][m % FJ], 0, 0, 0);
+      if (ks + 1 < KS) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-#ifndef KVR_PROBE_NO_MFMA
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
-#endif
+        for (int q = 0; q < NRD; ++q) {
+          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
         }
-      __builtin_amdgcn_sched_barrier(0);
-      if (ks + 1 < BK / 16) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          bfr[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(st + b_base[i] + ((cn ^ b_sw[i]) << 4));
+        for (int q = 0; q < NLOAD; ++q) {
+          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(SG_VMEM, 1, 0);
+        }
+        if (MF - NRD - NLOAD > 0) __builtin_amdgcn_sched_group_barrier(SG_MFMA, MF - NRD - NLOAD, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      } else {
+        // (MFMA, buffer load) x NLOAD, MFMAs up to PBAR; barrier; the first
+        // fragments of K tile kt+1 behind the remaining MFMAs, two per MFMA.
+        // On the last K tile the wait, the barrier and the reads are harmless
+        // leftovers.
+#pragma unroll
+        for (int q = 0; q < NLOAD; ++q) {
+          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(SG_VMEM, 1, 0);
+        }
+        if (PBAR - NLOAD > 0) __builtin_amdgcn_sched_group_barrier(SG_MFMA, PBAR - NLOAD, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        KVR_WAIT_VMCNT(LANDED);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        af[0][0] = *reinterpret_cast<const bf16x8*>(sta_n + a_base[0] + ((fhalf ^ a_sw[0]) << 4));
+#pragma unroll
+        for (int j = 0; j < FJ; ++j)
+          bfr[0][j] = *reinterpret_cast<const bf16x8*>(stb_n + b_base[j] + ((fhalf ^ b_sw[j]) << 4));
+#pragma unroll
+        for (int i = 1; i < FI; ++i)
+          af[0][i] = *reinterpret_cast<const bf16x8*>(sta_n + a_base[i] + ((fhalf ^ a_sw[i]) << 4));
+#pragma unroll
+        for (int m = PBAR; m < MF; ++m)
+          acc[m / FJ][m % FJ] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              af[cur][m / FJ], bfr[cur][m % FJ], acc[m / FJ][m % FJ], 0, 0, 0);
+#pragma unroll
+        for (int q = 0; q < NRD2; ++q) {
+          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 2, 0);
+        }
+        if (MF - PBAR - NRD2 > 0) __builtin_amdgcn_sched_group_barrier(SG_MFMA, MF - PBAR - NRD2, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 2; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-#ifndef KVR_PROBE_NO_MFMA
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
-#endif
-        }
-      __builtin_amdgcn_sched_barrier(0);
     }
   }
   KVR_WAIT_VMCNT(0);  // the trailing refetches land before the ring becomes the C tile
@@ -224,13 +358,13 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
     if (wm == pass) {
       // accumulator register r of tile (i, j): row 8*(r/4) + 4*(lane/32) + r%4, col lane%32
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < FI; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < FJ; ++j)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int row = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            const int col = wn * 128 + j * 32 + (lane & 31);
+            const int col = wn * (BN / WN) + j * 32 + (lane & 31);
             sC[row * LDC + col] = acc[i][j][r];
           }
     }
@@ -249,21 +383,17 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
 
 }  // namespace
 
-#ifndef KVR_GEMM_BK
-#define KVR_GEMM_BK 32
-#endif
-
 void launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = p.bmap == BMAP_GATEUP ? p.epi.ffn / (BN / 2) : (p.n_end - p.n_begin) / BN;
   const dim3 grid(tiles_m * tiles_n), block(NT);
   if (p.M <= 0 || tiles_n <= 0) return;
   if (epi == EPI_QKV)
-    hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, KVR_GEMM_BK>), grid, block, 0, s, p, tiles_m, tiles_n);
+    hipLaunchKernelGGL(gemm_bf16_kernel<EPI_QKV>, grid, block, 0, s, p, tiles_m, tiles_n);
   else if (epi == EPI_RESID)
-    hipLaunchKernelGGL((gemm_bf16_kernel<EPI_RESID, KVR_GEMM_BK>), grid, block, 0, s, p, tiles_m, tiles_n);
+    hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID>, grid, block, 0, s, p, tiles_m, tiles_n);
   else
-    hipLaunchKernelGGL((gemm_bf16_kernel<EPI_SWIGLU, KVR_GEMM_BK>), grid, block, 0, s, p, tiles_m, tiles_n);
+    hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU>, grid, block, 0, s, p, tiles_m, tiles_n);
 }
 
 }  // namespace kvr
