@@ -3,7 +3,7 @@
 // bf16 path (head_dim 128): a workgroup is 8 wave64s = HW q heads of one GQA
 // group x QW blocks of 32 queries of one request (HW * QW = 8), so every K/V
 // tile staged in LDS feeds 8 waves.  Key tiles of 64 keys stream into a
-// 3-stage LDS ring with global_load_lds_dwordx4 (two tiles in flight): K rows
+// 3-stage LDS ring with buffer_load_dwordx4 ... lds (two tiles in flight): K rows
 // from a contiguous per-head copy of the stored K, V from the V^T copy, both
 // written by the QKV epilogue with the values sent to the arena.  Scores are
 // computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: a lane owns
@@ -47,19 +47,27 @@ __device__ __forceinline__ int vsw(int d) { return (d & 7) ^ ((d >> 3) & 1); }
 #define KVR_WAIT_VMCNT(n) \
   __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (((n) >> 4) << 14) | (0x7 << 4) | (0xF << 8))
 
+constexpr int BUF_WORD3 = 0x00020000;  // gfx9 buffer descriptor: 32-bit data format
+
 // Issue this wave's share (2 K blocks + 2 V^T blocks of 1 KB) of key tile
-// starting at row kbase into ring stage `stage`.
+// starting at row kbase into ring stage `stage`.  Buffer loads with the LDS
+// bit are counted by vmcnt only, so the fragment reads from LDS keep exact
+// lgkm counts (global_load_lds would force lgkmcnt(0) before every MFMA).
+// k_voff / v_voff: this lane's byte offsets within the head's K copy / V^T
+// rows for key 0; the tile's key offset is scalar.
 __device__ __forceinline__ void issue_kv(char* smem, const bf16_t* Kc, const bf16_t* Vt,
-                                         int kbase, int stage, int wid, const int* k_row,
-                                         const int* k_off, const int* v_off) {
+                                         int head_bytes, int kbase, int stage, int wid,
+                                         const int* k_voff, const int* v_voff) {
   char* st = smem + stage * STAGE;
+  const auto rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(Kc), 0, head_bytes, BUF_WORD3);
+  const auto rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(Vt), 0, head_bytes, BUF_WORD3);
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int qk = wid + 8 * i;
-    __builtin_amdgcn_global_load_lds(Kc + (int64_t)(kbase + k_row[i]) * D + k_off[i],
-                                     (lds_void*)(st + qk * 1024), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(Vt + kbase + v_off[i], (lds_void*)(st + KTILE + qk * 1024), 16,
-                                     0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(st + qk * 1024), 16, k_voff[i],
+                                             kbase * D * 2, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(st + KTILE + qk * 1024), 16, v_voff[i],
+                                             kbase * 2, 0, 0);
   }
 }
 
@@ -78,7 +86,8 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   const int nkeys = q_start + q_len - req_start;
   const int ntiles = (nkeys + KB - 1) / KB;
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int qsub = wid / HW, h = kvh * g + hgrp * HW + wid % HW;
   const int half = lane >> 5, col = lane & 31;
   const bool wave_active = qsub * 32 < q_len;
@@ -102,15 +111,16 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
 
   // direct-to-LDS loaders: wave w issues K instructions w, w+8 (4 rows each) and
   // V^T instructions w, w+8 (8 rows each)
-  int k_row[2], k_off[2], v_off[2];
+  const int head_bytes = (int)(p.ldvt * D * 2);  // one head's K copy, and its V^T rows
+  int k_voff[2], v_voff[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int qk = wid + 8 * i;
     const int lr = 4 * qk + (lane >> 4);                  // LDS row
-    k_row[i] = ksig(lr);                                  // key held there
-    k_off[i] = ((lane & 15) ^ (lr & 15)) * 8;             // unit fetched into this slot
+    // key ksig(lr) lands there; unit (lane&15)^(lr&15) of it fills this lane's slot
+    k_voff[i] = (ksig(lr) * D + ((lane & 15) ^ (lr & 15)) * 8) * 2;
     const int dv = 8 * qk + (lane >> 3);
-    v_off[i] = dv * (int)p.ldvt + ((lane & 7) ^ vsw(dv)) * 8;
+    v_voff[i] = (dv * (int)p.ldvt + ((lane & 7) ^ vsw(dv)) * 8) * 2;
   }
 
   f32x16 acc_o[D / 32];
@@ -132,82 +142,107 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   }
   // key offset (within a 32-key half) of accumulator register r: ksig(8*(r/4) + 4*half + r%4)
 
-  issue_kv(smem, Kc, Vt, req_start, 0, wid, k_row, k_off, v_off);
-  issue_kv(smem, Kc, Vt, req_start + min(1, ntiles - 1) * KB, 1, wid, k_row, k_off, v_off);
+  issue_kv(smem, Kc, Vt, head_bytes, req_start, 0, wid, k_voff, v_voff);
+  issue_kv(smem, Kc, Vt, head_bytes, req_start + min(1, ntiles - 1) * KB, 1, wid, k_voff, v_voff);
   for (int kt = 0; kt < ntiles; ++kt) {
     KVR_WAIT_VMCNT(4);                      // this wave's loads of tile kt have landed
     __builtin_amdgcn_s_barrier();           // ... and every other wave's; stage of kt-1 is free
-    issue_kv(smem, Kc, Vt, req_start + min(kt + 2, ntiles - 1) * KB, (kt + 2) % NSTAGE, wid, k_row,
-             k_off, v_off);
+    issue_kv(smem, Kc, Vt, head_bytes, req_start + min(kt + 2, ntiles - 1) * KB, (kt + 2) % NSTAGE,
+             wid, k_voff, v_voff);
     const char* st = smem + (kt % NSTAGE) * STAGE;
 
     if (wave_active && kt * KB <= wave_last) {
-      // ---- S^T for keys [0,32) and [32,64) of the tile ----
+      // ---- S^T for keys [0,32) and [32,64) of the tile (the two accumulation
+      // chains alternate, so no MFMA waits on the one just issued) ----
       f32x16 s[2];
 #pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
+      for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[k2][r] = 0.0f;
-        const char* krow = st + (k2 * 32 + col) * 256;
 #pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
+      for (int ks = 0; ks < D / 16; ++ks)
+#pragma unroll
+        for (int k2 = 0; k2 < 2; ++k2) {
+          const char* krow = st + (k2 * 32 + col) * 256;
           const bf16x8 kf =
               *reinterpret_cast<const bf16x8*>(krow + (((2 * ks + half) ^ kslot0) << 4));
           s[k2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[k2], 0, 0, 0);
         }
+      // K fragment reads run four ahead of the MFMAs that consume them
+#pragma unroll
+      for (int q = 0; q < 4; ++q) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#pragma unroll
+      for (int q = 0; q < 12; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
-      // ---- scale, mask on diagonal tiles, online softmax ----
-      float mx = m_run;
-      if (kt * KB + KB - 1 > wave_first) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+      // ---- mask on diagonal tiles, online softmax ----
+      // The running max m_run lives in the log2 domain (scores times
+      // log2(e)/sqrt(d)); the scale is folded into the FMA that forms each
+      // exponent, and exp2 is the bare v_exp_f32 (results below 2^-126 flush
+      // to zero, far below bf16 resolution of P next to the row max's 1.0).
+      // The softmax is VALU work that competes with the matrix core for issue,
+      // so it is kept to one FMA, one exp, one add and half a convert per score.
+      if (__builtin_expect(kt * KB + KB - 1 > wave_first, 0)) {
+        // register r of half h holds tile key 32*k2 + ksig(8*(r/4) + 4h + r%4)
+        // = 32*k2 + 8h + kc(r): compare kc(r) with the lane's limit
+        const int lim = qpos - kt * KB - 8 * half;
 #pragma unroll
         for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int kpos = kt * KB + k2 * 32 + ksig(8 * (r >> 2) + 4 * half + (r & 3));
-            const float v = kpos <= qpos ? s[k2][r] * scale_log2 : -INFINITY;
-            s[k2][r] = v;
-            mx = fmaxf(mx, v);
-          }
-      } else {
-#pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const float v = s[k2][r] * scale_log2;
-            s[k2][r] = v;
-            mx = fmaxf(mx, v);
+            const int kc = 32 * k2 + 16 * ((r >> 3) & 1) + 4 * ((r >> 2) & 1) + (r & 3);
+            if (kc > lim) s[k2][r] = -INFINITY;
           }
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      float mx = s[0][0];
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[k2][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * scale_log2;
       if (__any(mx > m_run)) {
-        const float alpha = exp2f(m_run - mx);
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
         l_run *= alpha;
 #pragma unroll
         for (int t = 0; t < D / 32; ++t)
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc_o[t][r] *= alpha;
-        m_run = mx;
+        m_run = m_new;
       }
+      const float neg_m = -m_run;
       float lsum = 0.0f;
       bf16x8 pf[4];
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float e = exp2f(s[k2][r] - m_run);
+          const float e = __builtin_amdgcn_exp2f(fmaf(s[k2][r], scale_log2, neg_m));
           lsum += e;
           pf[k2 * 2 + (r >> 3)][r & 7] = (__bf16)e;
         }
       l_run += lsum;
-      // ---- O^T += V^T P^T; P^T slot j of chunk c is key 16c + 8*half + j ----
+      // ---- O^T += V^T P^T; P^T slot j of chunk c is key 16c + 8*half + j (the
+      // four d-tiles' chains alternate) ----
 #pragma unroll
-      for (int t = 0; t < D / 32; ++t)
+      for (int c = 0; c < 4; ++c)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
+        for (int t = 0; t < D / 32; ++t) {
           const bf16x8 vf = *reinterpret_cast<const bf16x8*>(st + vbase[t] +
                                                               (((2 * c + half) ^ vsw_l[t]) << 4));
           acc_o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[c], acc_o[t], 0, 0, 0);
         }
+      // V^T fragment reads run four ahead of their MFMAs
+#pragma unroll
+      for (int q = 0; q < 4; ++q) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#pragma unroll
+      for (int q = 0; q < 12; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
     }
   }
   KVR_WAIT_VMCNT(0);  // trailing refetches complete before the workgroup retires
