@@ -179,7 +179,8 @@ def main():
     T = wl.total_tokens
     wave = args.wave_tokens or min(T, 131072 if cfg != 5 else 65536)
     log(f"[bench] R={wl.num_requests} T={T} NB={wl.num_blocks} arena={wl.arena_bytes() / 2**30:.1f} GiB")
-    arena = Hn.DeviceArena(wl)
+    big = wl.arena_bytes() > (32 << 30)
+    arena = Hn.DeviceArena(wl, progress=log if big else None)
     arena.bind(0)
     ws, nbytes = Hn.alloc_workspace(shape, wl.num_requests, T, wave)
     stream = Hn.stream_ptr()
@@ -225,7 +226,7 @@ def main():
 
     check = None
     if not args.no_check:
-        check = arena.check_invariants()
+        check = arena.check_invariants(progress=log if big else None)
         log(f"[bench] arena invariants after the last rebuild: {check}")
 
     work = algorithmic_work(wl)

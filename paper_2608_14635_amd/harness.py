@@ -109,7 +109,8 @@ def host_copy_layer0(model: DeviceModel) -> Dict:
 class DeviceArena:
     """Arena tensor in the paged layout [L, 2, NB, B, nkv, d] (raw bits)."""
 
-    def __init__(self, wl: W.Workload, device="cuda", host_image: Optional[np.ndarray] = None):
+    def __init__(self, wl: W.Workload, device="cuda", host_image: Optional[np.ndarray] = None,
+                 progress=None):
         s = wl.shape
         self.wl = wl
         self.dt = s.dtype
@@ -126,7 +127,7 @@ class DeviceArena:
                 self.live_ref = self.bits[:, :, live].clone()
         else:
             self.bits = torch.empty(self.shape6, dtype=bits_t, device=device)
-            self.fill_initial()
+            self.fill_initial(progress)
         self.handle: Optional[int] = None
 
     @property
@@ -139,32 +140,58 @@ class DeviceArena:
     def sentinel(self) -> int:
         return _signed(W.SENTINEL_BITS[self.dt], self.dt)
 
+    def _chunk_blocks(self) -> int:
+        """Blocks per chunk so that one chunk of one plane is about 64 MiB."""
+        B, nkv, d = self.shape6[3:]
+        return max(1, (64 << 20) // (B * nkv * d * self.bits.element_size()))
+
+    def _base_pattern(self) -> torch.Tensor:
+        """Fixed finite bit pattern over the elements of one block."""
+        if getattr(self, "_base", None) is None:
+            B, nkv, d = self.shape6[3:]
+            e = torch.arange(B * nkv * d, device=self.bits.device, dtype=torch.int64)
+            h = (e * 2654435761 + 97531)
+            h = (h ^ (h >> 13)) * 1274126177
+            h = h ^ (h >> 16)
+            if self.dt == W.BF16:
+                bits = (h & 0x807F) | 0x3F80
+                bits = torch.where(bits >= 0x8000, bits - 0x10000, bits).to(torch.int16)
+            else:
+                bits = (h & 0x807FFFFF) | 0x3F800000
+                bits = torch.where(bits >= 0x80000000, bits - 0x100000000, bits).to(torch.int32)
+            self._base = bits
+        return self._base
+
     def live_pattern(self, blocks: torch.Tensor, layer_kv: int) -> torch.Tensor:
         """Deterministic finite bit patterns for other-live blocks, computed
-        on the device: [len(blocks), B, nkv, d]."""
+        on the device: [len(blocks), B, nkv, d].  A fixed per-element pattern
+        XOR a per-(block, layer, K|V) hash confined to the sign and mantissa
+        bits, so every value stays finite and the fill runs at copy speed."""
         B, nkv, d = self.shape6[3:]
-        e = torch.arange(B * nkv * d, device=blocks.device, dtype=torch.int64)
-        h = (blocks.to(torch.int64)[:, None] * 40503 + e[None, :] * 2654435761 + layer_kv * 97531)
-        h = (h ^ (h >> 13)) * 1274126177
+        h = blocks.to(torch.int64) * 40503 + layer_kv * 97531 + 12345
+        h = (h ^ (h >> 7)) * 1274126177
         h = h ^ (h >> 16)
         if self.dt == W.BF16:
-            bits = (h & 0x807F) | 0x3F80
-            bits = torch.where(bits >= 0x8000, bits - 0x10000, bits).to(torch.int16)
+            m = h & 0x807F
+            m = torch.where(m >= 0x8000, m - 0x10000, m).to(torch.int16)
         else:
-            bits = (h & 0x807FFFFF) | 0x3F800000
-            bits = torch.where(bits >= 0x80000000, bits - 0x100000000, bits).to(torch.int32)
-        return bits.view(len(blocks), B, nkv, d)
+            m = h & 0x807FFFFF
+            m = torch.where(m >= 0x80000000, m - 0x100000000, m).to(torch.int32)
+        return (self._base_pattern()[None, :] ^ m[:, None]).view(len(blocks), B, nkv, d)
 
-    def fill_initial(self) -> None:
+    def fill_initial(self, progress=None) -> None:
         self.bits.fill_(self.sentinel())
         live = torch.as_tensor(self.wl.other_live, device=self.bits.device)
         if live.numel() == 0:
             return
+        ch = self._chunk_blocks()
         for l in range(self.shape6[0]):
             for kv in range(2):
-                for i in range(0, live.numel(), 4096):
-                    blk = live[i:i + 4096]
+                for i in range(0, live.numel(), ch):
+                    blk = live[i:i + ch]
                     self.bits[l, kv, blk] = self.live_pattern(blk, 2 * l + kv)
+            if progress:
+                progress(f"fill layer {l + 1}/{self.shape6[0]}")
 
     def bind(self, device: int = 0) -> int:
         s = self.wl.shape
@@ -182,11 +209,11 @@ class DeviceArena:
         return a.view(np.uint16 if self.dt == W.BF16 else np.uint32).reshape(-1)
 
     # ---- invariants, checked on the device --------------------------------
-    def check_invariants(self) -> Dict[str, int]:
-        """Bit-exact checks at any size: unlisted blocks keep their fill
-        (sentinel or other-live pattern), tail slots of each request's last
-        block keep the sentinel, every written slot is finite and not the
-        sentinel.  Returns counts of violations per kind."""
+    def check_invariants(self, progress=None) -> Dict[str, int]:
+        """Bit-exact checks at any size, in chunks of about 64 MiB: unlisted
+        blocks keep their fill (sentinel or other-live pattern), tail slots of
+        each request's last block keep the sentinel, every written slot is
+        finite and not the sentinel.  Returns counts of violations per kind."""
         wl = self.wl
         dev = self.bits.device
         L, _, NB, B = self.shape6[:4]
@@ -196,10 +223,15 @@ class DeviceArena:
             if wl.num_requests else np.zeros(0, np.int32)
         ids_t = torch.as_tensor(ids.astype(np.int64), device=dev)
         listed[ids_t] = True
-        live = torch.as_tensor(wl.other_live, device=dev)
         is_live = torch.zeros(NB, dtype=torch.bool, device=dev)
-        if live.numel():
-            is_live[live] = True
+        if wl.other_live.size:
+            is_live[torch.as_tensor(wl.other_live, device=dev)] = True
+        live_index = None
+        if self.live_ref is not None:
+            # position of each other-live block within the snapshot
+            live_index = torch.full((NB,), -1, dtype=torch.int64, device=dev)
+            live_index[torch.as_tensor(wl.other_live, device=dev)] = torch.arange(
+                wl.other_live.size, device=dev)
         free = ~listed & ~is_live
         # tail slots: (block, slot) of last blocks with slot >= n % B
         tail_b, tail_s = [], []
@@ -214,27 +246,35 @@ class DeviceArena:
         tail_b = torch.as_tensor(tail_b, dtype=torch.int64, device=dev)
         tail_s = torch.as_tensor(tail_s, dtype=torch.int64, device=dev)
         sen = self.sentinel()
+        ch = self._chunk_blocks()
         bad = {"free_changed": 0, "live_changed": 0, "tail_changed": 0, "written_bad": 0}
         for l in range(L):
             for kv in range(2):
                 plane = self.bits[l, kv]
-                bad["free_changed"] += int((plane[free] != sen).sum())
-                if live.numel() and self.live_ref is not None:
-                    bad["live_changed"] += int((plane[live] != self.live_ref[l, kv]).sum())
-                elif live.numel():
-                    for i in range(0, live.numel(), 4096):
-                        blk = live[i:i + 4096]
-                        bad["live_changed"] += int((plane[blk] != self.live_pattern(blk, 2 * l + kv)).sum())
+                for c0 in range(0, NB, ch):
+                    c1 = min(NB, c0 + ch)
+                    sl = plane[c0:c1]
+                    fr = free[c0:c1]
+                    bad["free_changed"] += int(((sl != sen) & fr[:, None, None, None]).sum())
+                    lv = torch.nonzero(is_live[c0:c1]).flatten()
+                    if lv.numel():
+                        if live_index is not None:
+                            ref = self.live_ref[l, kv, live_index[lv + c0]]
+                        else:
+                            ref = self.live_pattern(lv + c0, 2 * l + kv)
+                        bad["live_changed"] += int((sl[lv] != ref).sum())
                 if tail_b.numel():
                     bad["tail_changed"] += int((plane[tail_b, tail_s] != sen).sum())
                 # written slots = slots of listed blocks except the tails: finite values
-                for i in range(0, ids_t.numel(), 8192):
-                    blk = ids_t[i:i + 8192]
+                for i in range(0, ids_t.numel(), ch):
+                    blk = ids_t[i:i + ch]
                     vals = plane[blk].view(_TORCH_VAL[self.dt])
                     bad["written_bad"] += int((~torch.isfinite(vals)).sum())
                 if tail_b.numel():
                     tails = plane[tail_b, tail_s].view(_TORCH_VAL[self.dt])
                     bad["written_bad"] -= int((~torch.isfinite(tails)).sum())
+            if progress:
+                progress(f"check layer {l + 1}/{L}")
         return bad
 
 
