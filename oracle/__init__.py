@@ -62,6 +62,13 @@ class Oracle:
             f.restype = C.c_int
             f.argtypes = [C.POINTER(_Model), C.c_void_p, C.POINTER(_Layer), I32P, I32P, C.c_int32,
                           I32P, C.c_int32, C.POINTER(_Arena), C.c_void_p]
+        self.lib.kvo_decode_step.restype = C.c_int
+        self.lib.kvo_decode_step.argtypes = [C.POINTER(_Model), C.c_void_p, C.POINTER(_Layer), I32P,
+                                             I32P, C.c_int32, I32P, C.c_int32, C.POINTER(_Arena),
+                                             C.c_void_p]
+        self.lib.kvo_logits.restype = C.c_int
+        self.lib.kvo_logits.argtypes = [C.POINTER(_Model), C.c_void_p, C.c_void_p, C.c_void_p,
+                                        C.c_int64, C.c_void_p]
         self.lib.kvo_layer0_kv.restype = C.c_int
         self.lib.kvo_layer0_kv.argtypes = [C.POINTER(_Model), C.c_void_p, C.POINTER(_Layer),
                                            I32P, I32P, C.c_int64, C.c_void_p, C.c_void_p]
@@ -125,6 +132,46 @@ class Oracle:
             raise ValueError("oracle rejected its arguments")
         return fh
 
+    def decode_step(self, shape, weights: Dict, tokens, positions, tables, arena: np.ndarray,
+                    block_size: int, num_blocks: int, dtype: Optional[int] = None,
+                    final_hidden: bool = True):
+        """One resumed-generation step in place on `arena`: token tokens[r] at
+        position positions[r] of request r.  Returns the final fp64 residual
+        [R, H] (needed for the logits) when final_hidden is set."""
+        dt = shape.dtype if dtype is None else dtype
+        m = self._model(shape, dt)
+        tokens, positions = self._i32(tokens), self._i32(positions)
+        tables = self._i32(tables)
+        R = tokens.shape[0]
+        assert positions.shape[0] == R and tables.ndim == 2 and tables.shape[0] == R
+        need = shape.num_layers * 2 * num_blocks * block_size * shape.num_kv_heads * shape.head_dim
+        assert arena.flags.c_contiguous and arena.size >= need, "arena smaller than its geometry"
+        ar = _Arena(arena.ctypes.data, block_size, num_blocks)
+        fh = np.zeros((R, shape.hidden), np.float64) if final_hidden else None
+        I32P = C.POINTER(C.c_int32)
+        rc = self.lib.kvo_decode_step(C.byref(m), self._check(weights["embed"], dt).ctypes.data,
+                                      self._layers(weights, dt), tokens.ctypes.data_as(I32P),
+                                      positions.ctypes.data_as(I32P), R,
+                                      tables.ctypes.data_as(I32P), tables.shape[1], C.byref(ar),
+                                      fh.ctypes.data if fh is not None else None)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        return fh
+
+    def logits(self, shape, head: Dict, hidden: np.ndarray, dtype: Optional[int] = None):
+        """Final RMSNorm + LM head of rows of the final residual: fp32 [n, vocab]."""
+        dt = shape.dtype if dtype is None else dtype
+        m = self._model(shape, dt)
+        hidden = np.ascontiguousarray(hidden, dtype=np.float64)
+        n = hidden.shape[0]
+        out = np.zeros((n, shape.vocab), np.float32)
+        rc = self.lib.kvo_logits(C.byref(m), self._check(head["final_norm"], dt).ctypes.data,
+                                 self._check(head["lm_head"], dt).ctypes.data,
+                                 hidden.ctypes.data, n, out.ctypes.data)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        return out
+
     def layer0_kv(self, shape, embed: np.ndarray, layer0: Dict, tokens, positions,
                   dtype: Optional[int] = None):
         dt = shape.dtype if dtype is None else dtype
@@ -163,6 +210,11 @@ class Oracle:
 
     def num_threads(self) -> int:
         return int(self.lib.kvo_num_threads())
+
+
+def greedy(logits: np.ndarray) -> np.ndarray:
+    """Greedy next tokens: the lowest index among equal maxima of each row."""
+    return np.argmax(np.asarray(logits), axis=-1).astype(np.int32)
 
 
 _default: Optional[Oracle] = None

@@ -335,6 +335,56 @@ int kvo_decode(const kvo_model* m, const void* embed, const kvo_layer* layers,
   return 0;
 }
 
+int kvo_decode_step(const kvo_model* m, const void* embed, const kvo_layer* layers,
+                    const int32_t* tokens, const int32_t* positions, int32_t num_requests,
+                    const int32_t* block_tables, int32_t max_blocks, kvo_arena* arena,
+                    double* final_hidden) {
+  int32_t r;
+  if (!m || num_requests < 0 || !arena || !arena->base || arena->block_size <= 0) return -1;
+  for (r = 0; r < num_requests; ++r) {
+    const int64_t p = positions[r];
+    int64_t b;
+    if (p < 0 || p / arena->block_size >= max_blocks) return -1;
+    if (tokens[r] < 0 || tokens[r] >= m->vocab) return -1;
+    for (b = 0; b <= p / arena->block_size; ++b) {
+      const int32_t blk = block_tables[(int64_t)r * max_blocks + b];
+      if (blk < 0 || blk >= arena->num_blocks) return -1;
+    }
+  }
+  for (r = 0; r < num_requests; ++r) {
+    const int64_t H = m->hidden;
+    const int32_t* table = block_tables + (int64_t)r * max_blocks;
+    double* x = (double*)malloc(sizeof(double) * (size_t)H);
+    double* scratch = (double*)malloc(sizeof(double) * scratch_elems(m, 1));
+    int l;
+    embed_rows(m, embed, tokens + r, 1, x);
+    for (l = 0; l < m->num_layers; ++l) {
+      const int kv_only = (l == m->num_layers - 1) && final_hidden == NULL;
+      layer_step(m, &layers[l], l, x, positions[r], 1, table, arena, kv_only, scratch);
+    }
+    if (final_hidden) memcpy(final_hidden + (int64_t)r * H, x, sizeof(double) * (size_t)H);
+    free(scratch);
+    free(x);
+  }
+  return 0;
+}
+
+int kvo_logits(const kvo_model* m, const void* final_norm, const void* lm_head,
+               const double* hidden, int64_t n, float* logits_out) {
+  const int64_t H = m ? m->hidden : 0, V = m ? m->vocab : 0;
+  double *a, *z;
+  int64_t i;
+  if (!m || !final_norm || !lm_head || !hidden || !logits_out || n < 0) return -1;
+  a = (double*)malloc(sizeof(double) * (size_t)(n * H + 1));
+  z = (double*)malloc(sizeof(double) * (size_t)(n * V + 1));
+  rmsnorm(hidden, final_norm, m->dtype, H, m->rms_eps, n, a);
+  project(lm_head, m->dtype, V, H, a, n, z);
+  for (i = 0; i < n * V; ++i) logits_out[i] = (float)z[i];
+  free(z);
+  free(a);
+  return 0;
+}
+
 int kvo_layer0_kv(const kvo_model* m, const void* embed, const kvo_layer* layer0,
                   const int32_t* tokens, const int32_t* positions, int64_t n, void* k_out,
                   void* v_out) {

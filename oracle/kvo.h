@@ -69,6 +69,23 @@ int kvo_decode(const kvo_model* m, const void* embed, const kvo_layer* layers,
                const int32_t* block_tables, int32_t max_blocks,
                kvo_arena* arena, double* final_hidden);
 
+/* One decode step of the resumed generation: token tokens[r] of request r at
+ * position positions[r], whose K/V for positions < positions[r] are already in
+ * the arena.  Writes its K/V at slot (table[p/B], p%B) in every layer and, if
+ * final_hidden is non-NULL ([R][hidden] fp64), the residual after the last
+ * layer (the paper's recoverability criterion: generation continues from the
+ * rebuilt state as from the original one, Sec. 4.2, Sec. 6). */
+int kvo_decode_step(const kvo_model* m, const void* embed, const kvo_layer* layers,
+                    const int32_t* tokens, const int32_t* positions, int32_t num_requests,
+                    const int32_t* block_tables, int32_t max_blocks, kvo_arena* arena,
+                    double* final_hidden);
+
+/* Final RMSNorm (gain final_norm, rounded like every norm output) and LM head
+ * lm_head [vocab, hidden]: logits_out[r][v] = fp32(sum_e W[v][e] a_r[e]), the
+ * sum in fp64, for n rows of the final residual stream. */
+int kvo_logits(const kvo_model* m, const void* final_norm, const void* lm_head,
+               const double* hidden, int64_t n, float* logits_out);
+
 /* Layer-0 rounded K and V rows (each num_kv_heads*head_dim elements of the
  * model dtype, written to k_out / v_out) for (token, position) pairs; layer 0
  * depends on nothing else, so sampled positions of a large batch can be

@@ -313,6 +313,18 @@ def host_weights(shape: ModelShape, seed: int = 11, gain_std: float = 0.1,
     return out
 
 
+def host_head_weights(shape: ModelShape, seed: int = 12, gain_std: float = 0.1,
+                      std: float = 0.02) -> Dict:
+    """Final RMSNorm gain (1 + N(0, gain_std)) and LM head [vocab, hidden]
+    (N(0, std)) for the resumed decode, from their own generator so that the
+    decoder weights of host_weights do not change."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    g = 1.0 + rng.standard_normal((shape.hidden,), dtype=np.float32) * np.float32(gain_std)
+    w = rng.standard_normal((shape.vocab, shape.hidden), dtype=np.float32) * np.float32(std)
+    return {"final_norm": _materialize(g.astype(np.float32), shape.dtype),
+            "lm_head": _materialize(w, shape.dtype)}
+
+
 def weights_as_f32(w: Dict, dtype: int) -> Dict:
     """Exact fp32 view of materialized weights (bf16 bits widened)."""
     conv = (lambda a: bf16_bits_to_f32(a)) if dtype == BF16 else (lambda a: a.astype(np.float32))

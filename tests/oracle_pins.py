@@ -407,6 +407,134 @@ def pin_empty_and_single(o):
     assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
 
 
+# ----------------------------------------------------------------------
+# resumed decode (the step after the rebuild): final norm, LM head, greedy
+# ----------------------------------------------------------------------
+def _head_in(head: dict, src_dt: int, dst_dt: int) -> dict:
+    if src_dt == dst_dt:
+        return head
+    f = {k: (W.bf16_bits_to_f32(v) if src_dt == BF16 else v.astype(np.float32)) for k, v in head.items()}
+    if dst_dt == F64:
+        return {k: v.astype(np.float64) for k, v in f.items()}
+    if dst_dt == F32:
+        return {k: v.astype(np.float32) for k, v in f.items()}
+    return {k: W.f32_to_bf16_bits(v) for k, v in f.items()}
+
+
+def pin_logits_torch(o):
+    """Final norm + LM head against the textbook torch formula, in the fp64
+    pin mode (no rounding) and with the bf16 rounding contract emulated."""
+    import torch_ref  # noqa: E402 - tests/ is on sys.path when pins run
+    shape = W.TINY_BF16
+    head = W.host_head_weights(shape, seed=31)
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((3, shape.hidden)) * 0.7
+    x32 = x.astype(np.float32).astype(np.float64)
+    z64 = o.logits(shape, _head_in(head, BF16, F64), x, dtype=F64)
+    t64 = torch_ref.logits(shape, head["final_norm"], head["lm_head"], x, BF16, None).numpy()
+    assert normwise(z64, t64) < 1e-6, normwise(z64, t64)
+    zb = o.logits(shape, head, x32)
+    tb = torch_ref.logits(shape, head["final_norm"], head["lm_head"], x32, BF16, "bf16").numpy()
+    # the normed activations are bf16: both sides round the same fp32 values
+    assert normwise(zb, tb) < 1e-5, normwise(zb, tb)
+
+
+def pin_logits_onehot_closed_form(o):
+    """A residual row c*e_k normalizes to a single entry g_k*c/sqrt(c^2/H+eps),
+    so every logit is one product: W[v][k] times that entry."""
+    shape = dataclasses.replace(W.TINY_F32, vocab=257)
+    head = W.host_head_weights(shape, seed=32)
+    H = shape.hidden
+    ks, cs = [3, 100, H - 1], [2.5, -0.75, 13.0]
+    x = np.zeros((len(ks), H))
+    for i, (k, c) in enumerate(zip(ks, cs)):
+        x[i, k] = c
+    z = o.logits(shape, head, x)
+    g = head["final_norm"].astype(np.float64)
+    wl = head["lm_head"].astype(np.float64)
+    for i, (k, c) in enumerate(zip(ks, cs)):
+        a = np.float64(np.float32(g[k] * c / math.sqrt(c * c / H + shape.rms_eps)))
+        expect = (wl[:, k] * a).astype(np.float32)
+        assert np.array_equal(z[i], expect), np.max(np.abs(z[i] - expect))
+
+
+def pin_greedy_lowest_index(o):
+    import oracle as _o
+    z = np.array([[1.0, 3.0, 3.0, -1.0], [0.0, 0.0, 0.0, 0.0], [-5.0, -4.0, -4.5, -4.0]], np.float32)
+    assert list(_o.greedy(z)) == [1, 0, 1]
+
+
+def _resume(o, shape, w, head, wl, prefix_mode, steps):
+    """Greedy continuation of every request of wl: its prefix (all but the last
+    token) rebuilt by prefill or fed token by token, then the last token and
+    each generated one decoded at the next position.  Returns (tokens
+    [steps, R], last logits, arena)."""
+    import oracle as _o
+    R = wl.num_requests
+    lens = wl.lens.astype(np.int64)
+    pre = dataclasses.replace(wl, lens=(lens - 1).astype(wl.lens.dtype),
+                              tokens=np.concatenate([wl.tokens[o0:o1 - 1] for o0, o1 in
+                                                     zip(wl.request_offsets()[:-1], wl.request_offsets()[1:])]))
+    a = W.host_arena(wl)
+    if prefix_mode == "prefill":
+        o.rebuild(shape, w, pre.tokens, pre.lens, pre.block_tables, a, wl.block_size, wl.num_blocks)
+    else:
+        for p in range(int(pre.lens.max())):
+            rs = [r for r in range(R) if p < pre.lens[r]]
+            toks = [pre.tokens[pre.request_offsets()[r] + p] for r in rs]
+            o.decode_step(shape, w, toks, [p] * len(rs), wl.block_tables[rs], a, wl.block_size,
+                          wl.num_blocks, final_hidden=False)
+    offs = wl.request_offsets()
+    cur = np.array([wl.tokens[offs[r + 1] - 1] for r in range(R)], np.int32)
+    pos = (lens - 1).astype(np.int32)
+    out, z = [], None
+    for _ in range(steps):
+        fh = o.decode_step(shape, w, cur, pos, wl.block_tables, a, wl.block_size, wl.num_blocks)
+        z = o.logits(shape, head, fh)
+        cur = _o.greedy(z)
+        out.append(cur.copy())
+        pos = pos + 1
+    return np.array(out), z, a
+
+
+def _resume_workload(shape, lens, steps, seed):
+    wl = W.small_workload(shape, [n + steps for n in lens], seed=seed, other_live_frac=0.0)
+    offs = wl.request_offsets()
+    toks = np.concatenate([wl.tokens[offs[r]:offs[r] + lens[r]] for r in range(len(lens))])
+    return dataclasses.replace(wl, lens=np.array(lens, dtype=wl.lens.dtype), tokens=toks)
+
+
+def pin_decode_step_chain_equals_decode(o):
+    """Stepping the oracle position by position over a request equals its
+    token-by-token decode mode, arena and final residual bit for bit."""
+    shape = W.TINY_F32
+    w = W.host_weights(shape, seed=33)
+    wl = W.small_workload(shape, [5, 19], seed=133, other_live_frac=0.0)
+    a_ref, fh_ref = run(o, shape, w, wl, mode="decode", final_hidden=True)
+    a = W.host_arena(wl)
+    offs = wl.request_offsets()
+    for r in range(wl.num_requests):
+        for p in range(int(wl.lens[r])):
+            fh = o.decode_step(shape, w, [wl.tokens[offs[r] + p]], [p], wl.block_tables[r:r + 1], a,
+                               wl.block_size, wl.num_blocks)
+            assert np.array_equal(fh[0], fh_ref[offs[r] + p])
+    assert np.array_equal(a, a_ref)
+
+
+def pin_resume_from_rebuild_equals_decode_built(o):
+    """The paper's recoverability criterion on the oracle: generation resumed
+    from a rebuilt (prefill) arena continues exactly as from the arena the
+    original token-by-token generation built."""
+    for shape in (W.TINY_F32, TINY_BF16_2L):
+        w = W.host_weights(shape, seed=34)
+        head = W.host_head_weights(shape, seed=35)
+        wl = _resume_workload(shape, [1, 6, 23], steps=5, seed=134)
+        t_re, z_re, a_re = _resume(o, shape, w, head, wl, "prefill", 5)
+        t_de, z_de, a_de = _resume(o, shape, w, head, wl, "decode", 5)
+        assert np.array_equal(t_re, t_de) and np.array_equal(z_re, z_de)
+        assert np.array_equal(a_re, a_de)
+
+
 PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
 
 

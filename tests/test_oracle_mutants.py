@@ -36,6 +36,14 @@ MUTANTS = [
     ("k_not_rotated", "rope_row(k + r * nkv * d, (int)nkv, (int)d, p, m->rope_theta, dt);", ";", 0),
     ("position_plus_one", "double phi = (double)pos * inv_freq;", "double phi = (double)(pos + 1) * inv_freq;", 0),
     ("no_rounding_of_q", "q[r * nq * d + e] = rnd(q[r * nq * d + e], dt);", "q[r * nq * d + e] = q[r * nq * d + e];", 0),
+    ("final_norm_gain_from_lm_head", "rmsnorm(hidden, final_norm, m->dtype, H, m->rms_eps, n, a);",
+     "rmsnorm(hidden, lm_head, m->dtype, H, m->rms_eps, n, a);", 0),
+    ("logits_of_unnormed_residual", "project(lm_head, m->dtype, V, H, a, n, z);",
+     "project(lm_head, m->dtype, V, H, hidden, n, z);", 0),
+    ("decode_step_position_plus_one", "layer_step(m, &layers[l], l, x, positions[r], 1, table, arena, kv_only, scratch);",
+     "layer_step(m, &layers[l], l, x, positions[r] + 1, 1, table, arena, kv_only, scratch);", 0),
+    ("decode_step_first_table", "const int32_t* table = block_tables + (int64_t)r * max_blocks;",
+     "const int32_t* table = block_tables;", 2),
 ]
 
 

@@ -93,3 +93,19 @@ def forward_batch(shape, w64, wl: W.Workload, rounding=None) -> List:
             continue
         out.append(forward(shape, w64, toks, rounding))
     return out
+
+
+def logits(shape: W.ModelShape, final_norm: np.ndarray, lm_head: np.ndarray, x: np.ndarray,
+           dtype: int, rounding: Optional[str] = None) -> torch.Tensor:
+    """Final RMSNorm + LM head of final residual rows x [n, H] (float64 in),
+    with the declared rounding of the norm output emulated as in forward()."""
+    conv = (lambda a: W.bf16_bits_to_f32(a)) if dtype == W.BF16 else (lambda a: a)
+    g, wl = _t(conv(final_norm)), _t(conv(lm_head))
+    a = F.rms_norm(_t(x), (shape.hidden,), weight=g, eps=float(shape.rms_eps))
+    if rounding is not None:
+        a = a.to(torch.float32)
+        if rounding == "bf16":
+            a = a.to(torch.bfloat16)
+        a = a.to(torch.float64)
+    z = F.linear(a, wl)
+    return z if rounding is None else z.to(torch.float32).to(torch.float64)
