@@ -61,6 +61,57 @@ def measured_traffic(kernel: str, workload: str):
     return rec.get("bytes_per_launch")
 
 
+def resume_decode(wl, model, arena, Hn, kvr, W, steps, stream, log):
+    """Resumed generation over the rebuilt arena: one greedy decode step per
+    request, timed with HIP events.  Each step decodes every request's last
+    prefix token again at its own position (rewriting that slot), so it
+    attends over the whole rebuilt context.  HBM-bound: the weights are read
+    once per step and every request's K/V context once per layer."""
+    import numpy as np
+    import torch
+    s = wl.shape
+    R = wl.num_requests
+    offs = wl.request_offsets()
+    lens = wl.lens.astype(np.int64)
+    live = lens > 0
+    rows = np.nonzero(live)[0]
+    toks = np.array([wl.tokens[offs[r + 1] - 1] for r in rows], np.int32)
+    pos = (lens[rows] - 1).astype(np.int32)
+    head = Hn.device_head_random(s, seed=0x5EED00FF)
+    nbytes = kvr.kv_decode_workspace_bytes(s, len(rows), int(pos.max()) + 1)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    nxt = torch.zeros(len(rows), dtype=torch.int32, device="cuda")
+
+    def step():
+        kvr.kv_decode_step(model.weights, head["final_norm"].data_ptr(), head["lm_head"].data_ptr(),
+                           toks, pos, wl.block_tables[rows], arena.handle, ws.data_ptr(), nbytes,
+                           nxt.data_ptr(), 0, stream)
+    step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    e = s.elem_bytes
+    H, F, d, nq, nkv, L = s.hidden, s.ffn_dim, s.head_dim, s.num_q_heads, s.num_kv_heads, s.num_layers
+    w_layer = (H * (nq + 2 * nkv) * d + nq * d * H + 3 * H * F + 2 * H) * e
+    weights = L * w_layer + (s.vocab * H + H) * e + len(rows) * H * e
+    kv_read = int(lens[rows].sum()) * L * 2 * nkv * d * e
+    kv_write = len(rows) * L * 2 * nkv * d * e
+    total = weights + kv_read + kv_write
+    out = {"steps": steps, "requests": int(len(rows)), "ms_per_step": ms,
+           "tokens_per_s": len(rows) / (ms / 1e3), "context_tokens": int(lens[rows].sum()),
+           "hbm_bytes_per_step": total, "achieved_GBps": total / (ms / 1e3) / 1e9,
+           "hbm_frac": total / (ms / 1e3) / 1e9 / PEAK_HBM_GBS,
+           "next_tokens": nxt.cpu().numpy().tolist()[:8]}
+    log(f"[bench] resume decode: {ms:.2f} ms per step of {len(rows)} requests, "
+        f"{out['achieved_GBps']:.0f} GB/s ({100 * out['hbm_frac']:.1f}% of HBM)")
+    return out
+
+
 def algorithmic_work(wl):
     """Flops and HBM bytes the method must spend (last layer: K/V projections only)."""
     s = wl.shape
@@ -135,6 +186,8 @@ def main():
     ap.add_argument("--wave-tokens", type=int, default=0, help="0 = largest that fits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
+    ap.add_argument("--decode-steps", type=int, default=4,
+                    help="resumed-decode steps timed after the rebuild (0 = none)")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="only copy this many bytes device-to-device (counter calibration)")
     args = ap.parse_args()
@@ -239,6 +292,10 @@ def main():
     gemm_ms = sum(prof[k]["ms"] for k in gemm_keys)
     gemm_tf = sum(prof[k]["flops"] for k in gemm_keys) / (gemm_ms / 1e3) / 1e12 if gemm_ms else 0.0
 
+    dec = None
+    if args.decode_steps > 0 and wl.num_requests > 0:
+        dec = resume_decode(wl, model, arena, Hn, kvr, W, args.decode_steps, stream, log)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
@@ -273,6 +330,7 @@ def main():
                                "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["ms"] and v["flops"] else None}
                            for k, v in prof.items()},
         "arena_check": check,
+        "resume_decode": dec,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

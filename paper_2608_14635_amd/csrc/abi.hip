@@ -1,6 +1,7 @@
 // C ABI of the KV-rebuild library: argument validation, wave planning,
-// metadata staging and the per-layer kernel sequence.  Host code only; the
-// kernels live in misc.hip, gemm_bf16.hip, gemm_f32.hip and attention.hip.
+// metadata staging and the per-layer kernel sequence of the rebuild and of the
+// resumed decode step.  Host code only; the kernels live in misc.hip,
+// gemm_bf16.hip, gemm_f32.hip, attention.hip and decode.hip.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -14,6 +15,7 @@
 #include <vector>
 
 #include "kvr.h"
+#include "kvr_decode.h"
 #include "kvr_profile.h"
 #include "launch.h"
 
@@ -238,6 +240,88 @@ kv_status check_request(const kv_model_desc* desc, int32_t B, int64_t NB, const 
   }
   if (total_out) *total_out = T;
   if (max_len_out) *max_len_out = max_len;
+  return KV_OK;
+}
+
+// Decode-step workspace: metadata first (one host->device copy), then the
+// per-request activations.  Block tables are staged up to the blocks a step
+// uses (at most max_position entries per request, the block size being 1 at
+// worst).  The final-norm rows are padded to a multiple of 256: they are the
+// B operand of the LM-head GEMM, whose output is the transposed logits
+// [vocab][npad].
+struct DecodeLayout {
+  int32_t R = 0, npad = 0, splits = 0;
+  int64_t max_position = 0;
+  size_t tok = 0, pos = 0, rowidx = 0, slot = 0, ctx = 0, tables = 0, meta_end = 0;
+  size_t rope = 0, x = 0, a = 0, q = 0, u = 0, hf = 0, part = 0, logit = 0, total = 0;
+};
+
+DecodeLayout make_decode_layout(const kv_model_desc& d, int32_t R, int64_t max_position) {
+  DecodeLayout L;
+  L.R = R;
+  L.max_position = max_position;
+  L.npad = (int32_t)round_up(std::max<int32_t>(R, 1), 256);
+  L.splits = decode_attn_splits(d.num_kv_heads, max_position);
+  const int64_t e = elem_bytes(d.dtype);
+  size_t off = 0;
+  auto seg = [&](size_t bytes) {
+    const size_t at = off;
+    off = (size_t)round_up((int64_t)(off + bytes), 256);
+    return at;
+  };
+  L.tok = seg(4 * (size_t)R);
+  L.pos = seg(4 * (size_t)R);
+  L.rowidx = seg(4 * (size_t)R);
+  L.slot = seg(8 * (size_t)R);
+  L.ctx = seg(4 * (size_t)R);
+  L.tables = seg(4 * (size_t)R * (size_t)max_position);
+  L.meta_end = off;
+  L.rope = seg((size_t)8 * R * (d.head_dim / 2));
+  L.x = seg((size_t)4 * R * d.hidden);
+  L.a = seg((size_t)e * L.npad * d.hidden);
+  L.q = seg((size_t)e * R * d.num_q_heads * d.head_dim);
+  L.u = seg((size_t)e * R * d.num_q_heads * d.head_dim);
+  L.hf = seg((size_t)e * R * d.ffn_dim);
+  L.part = seg((size_t)4 * R * d.num_q_heads * L.splits * (d.head_dim + 2));
+  L.logit = seg((size_t)4 * d.vocab * L.npad);
+  L.total = off;
+  return L;
+}
+
+kv_status check_decode(const kv_model_desc* desc, int32_t B, int64_t NB, const int32_t* tokens,
+                       const int32_t* positions, int32_t R, const int32_t* tables,
+                       int32_t max_blocks, int64_t* max_pos_out) {
+  kv_status st = check_desc(desc);
+  if (st != KV_OK) return st;
+  if (desc->num_q_heads / desc->num_kv_heads > 16 || desc->head_dim > 128)
+    return fail(KV_EINVAL, "decode supports at most 16 q heads per kv head and head_dim <= 128");
+  if (B <= 0 || NB <= 0) return fail(KV_EINVAL, "block_size and num_blocks must be positive");
+  if (R < 0) return fail(KV_EINVAL, "num_requests < 0");
+  if (max_blocks < 0) return fail(KV_EINVAL, "max_blocks_per_req < 0");
+  if (R > 0 && (!tokens || !positions || !tables))
+    return fail(KV_EINVAL, "null tokens, positions or block_tables");
+  int64_t max_pos = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    if (positions[r] < 0) return fail(KV_EINVAL, "positions[%d] = %d < 0", r, positions[r]);
+    if (tokens[r] < 0 || tokens[r] >= desc->vocab)
+      return fail(KV_ERANGE, "token %d of request %d outside [0, %d)", tokens[r], r, desc->vocab);
+    if (positions[r] / B >= max_blocks)
+      return fail(KV_ECAPACITY, "position %d of request %d needs block %d >= max_blocks_per_req %d",
+                  positions[r], r, positions[r] / B, max_blocks);
+    max_pos = std::max<int64_t>(max_pos, positions[r]);
+  }
+  std::vector<uint8_t> seen((size_t)NB, 0);
+  for (int32_t r = 0; r < R; ++r) {
+    for (int32_t b = 0; b <= positions[r] / B; ++b) {
+      const int32_t blk = tables[(int64_t)r * max_blocks + b];
+      if (blk < 0 || blk >= NB)
+        return fail(KV_ERANGE, "block_tables[%d][%d] = %d outside [0, %lld)", r, b, blk,
+                    (long long)NB);
+      if (seen[blk]) return fail(KV_EALIAS, "block %d listed twice", blk);
+      seen[blk] = 1;
+    }
+  }
+  if (max_pos_out) *max_pos_out = max_pos;
   return KV_OK;
 }
 
@@ -732,6 +816,239 @@ kv_status kv_rebuild(const kv_weights* w, const int32_t* tokens, const int32_t* 
     g_err = keep;
     return st;
   }
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// Resumed decode (kvr_decode.h)
+// ---------------------------------------------------------------------------
+uint64_t kv_decode_workspace_bytes(const kv_model_desc* desc, int32_t num_requests,
+                                   int64_t max_position) {
+  if (check_desc(desc) != KV_OK || num_requests <= 0 || max_position <= 0) return 0;
+  return make_decode_layout(*desc, num_requests, max_position).total;
+}
+
+kv_status kv_decode_check(const kv_model_desc* desc, int32_t block_size, int64_t num_blocks,
+                          const int32_t* tokens, const int32_t* positions, int32_t num_requests,
+                          const int32_t* block_tables, int32_t max_blocks_per_req) {
+  kv_status st = check_decode(desc, block_size, num_blocks, tokens, positions, num_requests,
+                              block_tables, max_blocks_per_req, nullptr);
+  return st == KV_OK ? ok() : st;
+}
+
+kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void* lm_head,
+                         const int32_t* tokens, const int32_t* positions, int32_t R,
+                         const int32_t* tables, int32_t max_blocks, kv_arena_t arena,
+                         void* workspace, uint64_t ws_bytes, void* stream, int32_t* next_tokens,
+                         float* logits) {
+  if (!live_arena(arena)) return fail(KV_ESTATE, "unknown or released arena handle");
+  if (!w || !w->embed || !w->layers) return fail(KV_EINVAL, "null weights");
+  const kv_model_desc& d = arena->desc;
+  if (!same_desc(w->desc, d)) return fail(KV_ESTATE, "weights and arena describe different models");
+  int64_t max_pos = 0;
+  kv_status st = check_decode(&d, arena->block_size, arena->num_blocks, tokens, positions, R, tables,
+                              max_blocks, &max_pos);
+  if (st != KV_OK) return st;
+  if (R == 0) return ok();
+  if (!final_norm || !lm_head) return fail(KV_EINVAL, "null final_norm or lm_head");
+  if (!next_tokens) return fail(KV_EINVAL, "null next_tokens");
+  for (int l = 0; l < d.num_layers; ++l) {
+    const kv_layer_weights& lw = w->layers[l];
+    if (!lw.attn_norm || !lw.wq || !lw.wk || !lw.wv || !lw.wo || !lw.ffn_norm || !lw.w_gate ||
+        !lw.w_up || !lw.w_down)
+      return fail(KV_EINVAL, "null weight pointer in layer %d", l);
+  }
+  if (!workspace) return fail(KV_EINVAL, "null workspace");
+  const DecodeLayout L = make_decode_layout(d, R, max_pos + 1);
+  if (L.total > ws_bytes)
+    return fail(KV_ENOMEM, "workspace of %llu bytes < %llu needed", (unsigned long long)ws_bytes,
+                (unsigned long long)L.total);
+  DeviceGuard dg(arena->device);
+  if (dg.err != hipSuccess) return fail(KV_EDEVICE, "cannot select device %d", arena->device);
+  {
+    const hipError_t pre = hipGetLastError();
+    if (pre != hipSuccess) return fail(KV_EDEVICE, "pending device error: %s", hipGetErrorString(pre));
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  char* ws = reinterpret_cast<char*>(workspace);
+  const int32_t B = arena->block_size;
+
+  // ---- stage metadata through the arena's pinned buffer ----
+  if (arena->staged_pending) {
+    (void)hipEventSynchronize(arena->staged);
+    arena->staged_pending = false;
+  }
+  if (arena->pinned_bytes < L.meta_end) {
+    if (arena->pinned) (void)hipHostFree(arena->pinned);
+    arena->pinned = nullptr;
+    arena->pinned_bytes = 0;
+    if (hipHostMalloc(&arena->pinned, L.meta_end, hipHostMallocDefault) != hipSuccess) {
+      arena->pinned = nullptr;
+      return fail(KV_ENOMEM, "pinned staging allocation of %zu bytes failed", (size_t)L.meta_end);
+    }
+    arena->pinned_bytes = L.meta_end;
+  }
+  char* hb = reinterpret_cast<char*>(arena->pinned);
+  int32_t* htok = reinterpret_cast<int32_t*>(hb + L.tok);
+  int32_t* hpos = reinterpret_cast<int32_t*>(hb + L.pos);
+  int32_t* hrow = reinterpret_cast<int32_t*>(hb + L.rowidx);
+  int64_t* hslot = reinterpret_cast<int64_t*>(hb + L.slot);
+  int32_t* hctx = reinterpret_cast<int32_t*>(hb + L.ctx);
+  int32_t* htab = reinterpret_cast<int32_t*>(hb + L.tables);
+  const int32_t tab_ld = (int32_t)(max_pos / B + 1);  // staged table entries per request
+  for (int32_t r = 0; r < R; ++r) {
+    const int32_t p = positions[r];
+    const int32_t* tab = tables + (int64_t)r * max_blocks;
+    htok[r] = tokens[r];
+    hpos[r] = p;
+    hrow[r] = r;
+    hslot[r] = (int64_t)tab[p / B] * B + p % B;
+    hctx[r] = p + 1;
+    for (int32_t b = 0; b < tab_ld; ++b) htab[(int64_t)r * tab_ld + b] = b <= p / B ? tab[b] : 0;
+  }
+  {
+    const size_t meta_bytes = L.tables + (size_t)4 * R * tab_ld;
+    hipError_t e = hipMemcpyAsync(ws, hb, meta_bytes, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipEventRecord(arena->staged, s);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(KV_EDEVICE, "metadata upload failed: %s", hipGetErrorString(e));
+    }
+    arena->staged_pending = true;
+  }
+
+  const int dt = d.dtype;
+  const int64_t e = elem_bytes(dt);
+  const int H = d.hidden, nq = d.num_q_heads, nkv = d.num_kv_heads, hd = d.head_dim, F = d.ffn_dim;
+  const float eps = (float)d.rms_eps;
+  const int64_t plane = arena->num_blocks * (int64_t)B * nkv * hd;  // elements
+  char* abase = reinterpret_cast<char*>(arena->base);
+  const int32_t* d_tok = reinterpret_cast<const int32_t*>(ws + L.tok);
+  const int32_t* d_pos = reinterpret_cast<const int32_t*>(ws + L.pos);
+  const int32_t* d_row = reinterpret_cast<const int32_t*>(ws + L.rowidx);
+  const int64_t* d_slot = reinterpret_cast<const int64_t*>(ws + L.slot);
+  const int32_t* d_ctx = reinterpret_cast<const int32_t*>(ws + L.ctx);
+  const int32_t* d_tab = reinterpret_cast<const int32_t*>(ws + L.tables);
+  float2* rope = reinterpret_cast<float2*>(ws + L.rope);
+  float* X = reinterpret_cast<float*>(ws + L.x);
+  void* A = ws + L.a;
+  void* Q = ws + L.q;
+  void* U = ws + L.u;
+  void* HF = ws + L.hf;
+  float* part = reinterpret_cast<float*>(ws + L.part);
+  float* logit_t = reinterpret_cast<float*>(ws + L.logit);
+  auto gemm = dt == KV_BF16 ? launch_gemm_bf16 : launch_gemm_f32;
+  (void)e;
+
+  // rope rows of the step's positions; the QKV epilogue indexes them by row
+  launch_rope_rows(rope, d_pos, R, hd, d.rope_theta, s);
+  launch_embed_norm(dt, w->embed, d_tok, w->layers[0].attn_norm, X, A, R, H, eps, s);
+  for (int l = 0; l < d.num_layers; ++l) {
+    const kv_layer_weights& lw = w->layers[l];
+    if (l > 0) launch_rmsnorm(dt, X, lw.attn_norm, A, R, H, eps, s);
+    char* plane_k = abase + (int64_t)(2 * l) * plane * elem_bytes(dt);
+    char* plane_v = abase + (int64_t)(2 * l + 1) * plane * elem_bytes(dt);
+    GemmParams g{};
+    g.A = A;
+    g.lda = H;
+    g.M = R;
+    g.K = H;
+    g.B0 = lw.wq;
+    g.B1 = lw.wk;
+    g.B2 = lw.wv;
+    g.bmap = BMAP_QKV;
+    g.s0 = nq * hd;
+    g.s1 = nq * hd + nkv * hd;
+    g.n_begin = 0;
+    g.n_end = (nq + 2 * nkv) * hd;
+    g.epi.q_out = Q;
+    g.epi.arena_k = plane_k;
+    g.epi.arena_v = plane_v;
+    g.epi.vt = nullptr;
+    g.epi.kc = nullptr;
+    g.epi.ldvt = 0;
+    g.epi.slot = d_slot;
+    g.epi.pos = d_row;
+    g.epi.rope = rope;
+    g.epi.nq = nq;
+    g.epi.nkv = nkv;
+    g.epi.d = hd;
+    gemm(EPI_QKV, g, s);
+
+    DecodeAttnParams ap{};
+    ap.q = Q;
+    ap.plane_k = plane_k;
+    ap.plane_v = plane_v;
+    ap.tables = d_tab;
+    ap.max_blocks = tab_ld;
+    ap.block_size = B;
+    ap.ctx = d_ctx;
+    ap.nq = nq;
+    ap.nkv = nkv;
+    ap.d = hd;
+    ap.splits = L.splits;
+    ap.part = part;
+    ap.out = U;
+    launch_decode_attention(dt, ap, R, s);
+
+    GemmParams go{};
+    go.A = U;
+    go.lda = nq * hd;
+    go.M = R;
+    go.K = nq * hd;
+    go.B0 = lw.wo;
+    go.bmap = BMAP_PLAIN;
+    go.n_begin = 0;
+    go.n_end = H;
+    go.epi.x = X;
+    go.epi.ldx = H;
+    gemm(EPI_RESID, go, s);
+    launch_rmsnorm(dt, X, lw.ffn_norm, A, R, H, eps, s);
+    GemmParams gu{};
+    gu.A = A;
+    gu.lda = H;
+    gu.M = R;
+    gu.K = H;
+    gu.B0 = lw.w_gate;
+    gu.B1 = lw.w_up;
+    gu.bmap = BMAP_GATEUP;
+    gu.n_begin = 0;
+    gu.n_end = 2 * F;
+    gu.epi.hf = HF;
+    gu.epi.ldh = F;
+    gu.epi.ffn = F;
+    gemm(EPI_SWIGLU, gu, s);
+    GemmParams gd{};
+    gd.A = HF;
+    gd.lda = F;
+    gd.M = R;
+    gd.K = F;
+    gd.B0 = lw.w_down;
+    gd.bmap = BMAP_PLAIN;
+    gd.n_begin = 0;
+    gd.n_end = H;
+    gd.epi.x = X;
+    gd.epi.ldx = H;
+    gemm(EPI_RESID, gd, s);
+  }
+  // final norm, LM head (transposed: vocab rows x padded request columns), argmax
+  launch_rmsnorm(dt, X, final_norm, A, R, H, eps, s);
+  GemmParams gl{};
+  gl.A = lm_head;
+  gl.lda = H;
+  gl.M = d.vocab;
+  gl.K = H;
+  gl.B0 = A;
+  gl.ldb = H;
+  gl.bmap = BMAP_PLAIN;
+  gl.n_begin = 0;
+  gl.n_end = dt == KV_BF16 ? L.npad : R;
+  gl.epi.x = logit_t;
+  gl.epi.ldx = L.npad;
+  gemm(EPI_STORE, gl, s);
+  launch_argmax(logit_t, L.npad, d.vocab, R, next_tokens, logits, s);
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(KV_EDEVICE, "kernel launch failed: %s", hipGetErrorString(err));
   return ok();
 }
 

@@ -1,0 +1,268 @@
+// Kernels of the resumed decode step (one new token per request over the
+// rebuilt arena): the RoPE rows of the step's positions, paged split-K decode
+// attention with its fixed-order combine, and the greedy argmax over the LM
+// head's logits.
+//
+// Decode attention reads K and V straight from the paged arena: key j of
+// request r lives at slot table[r][j/B]*B + j%B of the layer's K and V planes.
+// A workgroup (4 waves) takes one (request, kv head, key range) and all g q
+// heads of that kv head.  Per block of 64 keys it stages the K and V rows in
+// LDS (coalesced 16-byte loads of whole rows), computes the g x 64 scores with
+// one key per lane (row pitch padded by 16 bytes, so 16-lane LDS phases hit
+// distinct banks), runs the online softmax per head in the exp2 domain (one
+// wave owns a head's running max and sum), and accumulates P.V with threads
+// over (head, dim).  Each split writes (m, l, o[d]) partials; a second kernel
+// merges the splits in index order, so results do not depend on timing.
+// The step is HBM-bound on the context's K/V reads.
+#include <algorithm>
+
+#include "common.h"
+#include "launch.h"
+
+namespace kvr {
+
+namespace {
+
+constexpr int DKB = 64;    // keys per staged block
+constexpr int DNT = 256;   // 4 waves
+constexpr int DMAXG = 16;  // q heads per kv head supported
+constexpr int DMAXD = 128;
+
+__global__ void rope_rows_kernel(float2* table, const int32_t* positions, int rows, int half,
+                                 double theta, int d) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)rows * half) return;
+  const int r = (int)(idx / half), i = (int)(idx % half);
+  const double inv_freq = pow(theta, -(double)(2 * i) / (double)d);
+  const double phi = (double)positions[r] * inv_freq;
+  table[idx] = make_float2((float)cos(phi), (float)sin(phi));
+}
+
+__device__ __forceinline__ void load_vals8(const float* p, float* v) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void load_vals8(const bf16_t* p, float* v) {
+  const uint4 u = *reinterpret_cast<const uint4*>(p);
+  v[0] = __uint_as_float(u.x << 16); v[1] = __uint_as_float(u.x & 0xffff0000u);
+  v[2] = __uint_as_float(u.y << 16); v[3] = __uint_as_float(u.y & 0xffff0000u);
+  v[4] = __uint_as_float(u.z << 16); v[5] = __uint_as_float(u.z & 0xffff0000u);
+  v[6] = __uint_as_float(u.w << 16); v[7] = __uint_as_float(u.w & 0xffff0000u);
+}
+
+template <typename T>
+__global__ __launch_bounds__(DNT) void decode_attn_kernel(DecodeAttnParams p) {
+  constexpr int PITCH = DMAXD * (int)sizeof(T) + 16;  // bytes per staged row
+  __shared__ __attribute__((aligned(16))) char sk[DKB * PITCH];
+  __shared__ __attribute__((aligned(16))) char sv[DKB * PITCH];
+  __shared__ float sq[DMAXG * DMAXD];
+  __shared__ float sp[DMAXG * DKB];
+  __shared__ float s_m[DMAXG], s_l[DMAXG], s_alpha[DMAXG];
+
+  const int S = p.splits;
+  int bid = blockIdx.x;
+  const int split = bid % S;
+  bid /= S;
+  const int kvh = bid % p.nkv, r = bid / p.nkv;
+  const int g = p.nq / p.nkv, d = p.d;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int ctx = p.ctx[r];
+  const int chunk = ((ctx + S - 1) / S + DKB - 1) / DKB * DKB;
+  const int k0 = split * chunk, k1 = min(ctx, k0 + chunk);
+  const float scale_log2 = 1.4426950408889634f / sqrtf((float)d);
+  const int64_t row_elems = (int64_t)p.nkv * d;  // one token slot of a plane
+
+  // queries of the g heads, fp32
+  const T* qsrc = reinterpret_cast<const T*>(p.q) + (int64_t)r * p.nq * d + (int64_t)kvh * g * d;
+  for (int i = tid; i < g * d; i += DNT) sq[i] = Elem<T>::load(qsrc, i);
+  if (tid < g) {
+    s_m[tid] = -INFINITY;
+    s_l[tid] = 0.0f;
+  }
+  // P.V outputs of this thread: (head, dim) pairs o = tid + DNT * j
+  constexpr int OMAX = DMAXG * DMAXD / DNT;
+  float acc[OMAX];
+#pragma unroll
+  for (int j = 0; j < OMAX; ++j) acc[j] = 0.0f;
+  const int* table = p.tables + (int64_t)r * p.max_blocks;
+  const T* Kp = reinterpret_cast<const T*>(p.plane_k);
+  const T* Vp = reinterpret_cast<const T*>(p.plane_v);
+  const int units = d * (int)sizeof(T) / 16;  // 16-byte units per row
+  __syncthreads();
+
+  for (int kb = k0; kb < k1; kb += DKB) {
+    // ---- stage K and V rows of keys kb .. kb+63 (zeros past k1) ----
+    for (int i = tid; i < DKB * units; i += DNT) {
+      const int key = i / units, u = i % units;
+      const int j = kb + key;
+      uint4 kvv = make_uint4(0, 0, 0, 0), vvv = make_uint4(0, 0, 0, 0);
+      if (j < k1) {
+        const int64_t slot = (int64_t)table[j / p.block_size] * p.block_size + j % p.block_size;
+        const int64_t off = slot * row_elems + (int64_t)kvh * d;
+        kvv = reinterpret_cast<const uint4*>(Kp + off)[u];
+        vvv = reinterpret_cast<const uint4*>(Vp + off)[u];
+      }
+      *reinterpret_cast<uint4*>(sk + key * PITCH + u * 16) = kvv;
+      *reinterpret_cast<uint4*>(sv + key * PITCH + u * 16) = vvv;
+    }
+    __syncthreads();
+    // ---- scores: one key per lane, heads h = wid, wid+4, ... ----
+    const bool kvalid = kb + lane < k1;
+    for (int h = wid; h < g; h += DNT / 64) {
+      float s = 0.0f;
+      const T* krow = reinterpret_cast<const T*>(sk + lane * PITCH);
+      const float* qh = sq + h * d;
+      for (int e = 0; e < d; e += 8) {
+        float kv8[8];
+        load_vals8(krow + e, kv8);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s = fmaf(qh[e + i], kv8[i], s);
+      }
+      s = kvalid ? s * scale_log2 : -INFINITY;
+      float mx = s;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+      const float m_old = s_m[h];
+      const float m_new = fmaxf(m_old, mx);
+      const float e = __builtin_amdgcn_exp2f(s - m_new);
+      const float sum = wave_sum(e);
+      sp[h * DKB + lane] = e;
+      if (lane == 0) {
+        const float alpha = __builtin_amdgcn_exp2f(m_old - m_new);
+        s_alpha[h] = alpha;
+        s_l[h] = s_l[h] * alpha + sum;
+        s_m[h] = m_new;
+      }
+    }
+    __syncthreads();
+    // ---- O = O * alpha + P.V over the block's keys ----
+#pragma unroll
+    for (int j = 0; j < OMAX; ++j) {
+      const int o = tid + DNT * j;
+      if (o < g * d) {
+        const int h = o / d, e = o % d;
+        float a = acc[j] * s_alpha[h];
+        const float* ph = sp + h * DKB;
+        for (int key = 0; key < DKB; ++key)
+          a = fmaf(ph[key], Elem<T>::load(reinterpret_cast<const T*>(sv + key * PITCH), e), a);
+        acc[j] = a;
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- partials: [r][h][split][d + 2] = o[0..d), m, l ----
+  const int stride = d + 2;
+#pragma unroll
+  for (int j = 0; j < OMAX; ++j) {
+    const int o = tid + DNT * j;
+    if (o < g * d) {
+      const int h = o / d, e = o % d;
+      const int hq = kvh * g + h;
+      p.part[(((int64_t)r * p.nq + hq) * S + split) * stride + e] = acc[j];
+    }
+  }
+  if (tid < g) {
+    const int hq = kvh * g + tid;
+    float* tail = p.part + (((int64_t)r * p.nq + hq) * S + split) * stride + d;
+    tail[0] = s_m[tid];
+    tail[1] = s_l[tid];
+  }
+}
+
+// Merge the splits of one (request, q head) in split order; round to T.
+template <typename T>
+__global__ __launch_bounds__(DMAXD) void decode_combine_kernel(DecodeAttnParams p) {
+  const int r = blockIdx.x / p.nq, h = blockIdx.x % p.nq;
+  const int e = threadIdx.x, d = p.d, S = p.splits, stride = d + 2;
+  const float* base = p.part + ((int64_t)r * p.nq + h) * S * stride;
+  float M = -INFINITY;
+  for (int s = 0; s < S; ++s) M = fmaxf(M, base[s * stride + d]);
+  float L = 0.0f, o = 0.0f;
+  for (int s = 0; s < S; ++s) {
+    const float w = __builtin_amdgcn_exp2f(base[s * stride + d] - M);
+    L = fmaf(base[s * stride + d + 1], w, L);
+    if (e < d) o = fmaf(base[s * stride + e], w, o);
+  }
+  if (e < d) {
+    T* out = reinterpret_cast<T*>(p.out) + (int64_t)r * p.nq * d + (int64_t)h * d;
+    Elem<T>::store(out, e, o / L);
+  }
+}
+
+// Greedy token of request r from the transposed logits [vocab][ld]: the
+// largest value, the lowest index among equal ones; optionally the logits
+// row [r][vocab] copied out.
+__global__ __launch_bounds__(256) void argmax_kernel(const float* logits_t, int64_t ld, int vocab,
+                                                     int32_t* next_tokens, float* logits_out) {
+  __shared__ float sv[256];
+  __shared__ int si[256];
+  const int r = blockIdx.x, t = threadIdx.x;
+  float best = -INFINITY;
+  int bi = -1;
+  for (int v = t; v < vocab; v += 256) {
+    const float z = logits_t[(int64_t)v * ld + r];
+    if (logits_out) logits_out[(int64_t)r * vocab + v] = z;
+    if (bi < 0 || z > best) {
+      best = z;
+      bi = v;
+    }
+  }
+  sv[t] = best;
+  si[t] = bi;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) {
+      const float a = sv[t], b = sv[t + w];
+      const int ia = si[t], ib = si[t + w];
+      if (ib >= 0 && (ia < 0 || b > a || (b == a && ib < ia))) {
+        sv[t] = b;
+        si[t] = ib;
+      }
+    }
+    __syncthreads();
+  }
+  if (t == 0) next_tokens[r] = si[0] < 0 ? 0 : si[0];
+}
+
+}  // namespace
+
+void launch_rope_rows(float2* table, const int32_t* positions, int rows, int d, double theta,
+                      hipStream_t s) {
+  const int half = d / 2;
+  const int64_t n = (int64_t)rows * half;
+  if (n <= 0) return;
+  hipLaunchKernelGGL(rope_rows_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, table,
+                     positions, rows, half, theta, d);
+}
+
+int decode_attn_splits(int nkv, int64_t max_ctx) {
+  // about 1024 workgroups per request, at least 256 keys per split; independent
+  // of the request count, so a workspace sized for R requests fits any fewer
+  const int64_t want = (1024 + nkv - 1) / nkv;
+  const int64_t cap = (max_ctx + 255) / 256;
+  return (int)std::max<int64_t>(1, std::min(want, cap));
+}
+
+void launch_decode_attention(int dtype, const DecodeAttnParams& p, int num_requests,
+                             hipStream_t s) {
+  if (num_requests <= 0) return;
+  const dim3 grid((unsigned)((int64_t)num_requests * p.nkv * p.splits));
+  const dim3 cgrid((unsigned)((int64_t)num_requests * p.nq));
+  if (dtype == 1) {
+    hipLaunchKernelGGL(decode_attn_kernel<bf16_t>, grid, dim3(DNT), 0, s, p);
+    hipLaunchKernelGGL(decode_combine_kernel<bf16_t>, cgrid, dim3(DMAXD), 0, s, p);
+  } else {
+    hipLaunchKernelGGL(decode_attn_kernel<float>, grid, dim3(DNT), 0, s, p);
+    hipLaunchKernelGGL(decode_combine_kernel<float>, cgrid, dim3(DMAXD), 0, s, p);
+  }
+}
+
+void launch_argmax(const float* logits_t, int64_t ld, int vocab, int num_requests,
+                   int32_t* next_tokens, float* logits_out, hipStream_t s) {
+  if (num_requests <= 0) return;
+  hipLaunchKernelGGL(argmax_kernel, dim3(num_requests), dim3(256), 0, s, logits_t, ld, vocab,
+                     next_tokens, logits_out);
+}
+
+}  // namespace kvr

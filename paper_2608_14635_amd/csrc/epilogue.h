@@ -8,6 +8,7 @@
 //            dtype, Q rows to the workspace, K and V rows scattered to their
 //            arena slots, and V^T columns for the attention kernel;
 //   RESID  : X += acc on the fp32 residual stream;
+//   STORE  : X = acc (the transposed logits of the decode step's LM head);
 //   SWIGLU : h = silu(gate) * up from the two column halves of the tile.
 #pragma once
 #include "common.h"
@@ -119,6 +120,22 @@ __device__ __forceinline__ void epi_resid(const float* sC, int ldc, int rows, in
     xv.z += src[2];
     xv.w += src[3];
     *xp = xv;
+  }
+}
+
+// STORE: X = acc (fp32), columns [n0, n0 + BN) of rows < M.
+template <int BN, int NT>
+__device__ __forceinline__ void epi_store(const float* sC, int ldc, int rows, int m_base, int M,
+                                          int n0, const EpiParams& e) {
+  const int tid = threadIdx.x;
+  const int per_row = BN / 4;
+  for (int it = tid; it < rows * per_row; it += NT) {
+    const int r = it / per_row, c0 = (it % per_row) * 4;
+    const int m = m_base + r;
+    if (m >= M) continue;
+    const float* src = sC + (int64_t)r * ldc + c0;
+    *reinterpret_cast<float4*>(e.x + (int64_t)m * e.ldx + n0 + c0) =
+        make_float4(src[0], src[1], src[2], src[3]);
   }
 }
 

@@ -374,6 +374,8 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
       epi_qkv<bf16_t, BN, NT>(sC, LDC, 128, m_base, p.M, p.n_begin + tile_n * BN, p.epi);
     } else if (EPI == EPI_RESID) {
       epi_resid<BN, NT>(sC, LDC, 128, m_base, p.M, p.n_begin + tile_n * BN, p.epi);
+    } else if (EPI == EPI_STORE) {
+      epi_store<BN, NT>(sC, LDC, 128, m_base, p.M, p.n_begin + tile_n * BN, p.epi);
     } else {
       epi_swiglu<bf16_t, BN, NT>(sC, LDC, 128, m_base, p.M, tile_n * (BN / 2), p.epi);
     }
@@ -392,6 +394,8 @@ void launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
     hipLaunchKernelGGL(gemm_bf16_kernel<EPI_QKV>, grid, block, 0, s, p, tiles_m, tiles_n);
   else if (epi == EPI_RESID)
     hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID>, grid, block, 0, s, p, tiles_m, tiles_n);
+  else if (epi == EPI_STORE)
+    hipLaunchKernelGGL(gemm_bf16_kernel<EPI_STORE>, grid, block, 0, s, p, tiles_m, tiles_n);
   else
     hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU>, grid, block, 0, s, p, tiles_m, tiles_n);
 }

@@ -88,6 +88,8 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmParams p, int tiles_n)
     epi_qkv<float, BN, NT>(sC, LDC, BM, m0, p.M, p.n_begin + tile_n * BN, p.epi);
   else if (EPI == EPI_RESID)
     epi_resid<BN, NT>(sC, LDC, BM, m0, p.M, p.n_begin + tile_n * BN, p.epi);
+  else if (EPI == EPI_STORE)
+    epi_store<BN, NT>(sC, LDC, BM, m0, p.M, p.n_begin + tile_n * BN, p.epi);
   else
     epi_swiglu<float, BN, NT>(sC, LDC, BM, m0, p.M, tile_n * (BN / 2), p.epi);
 }
@@ -104,6 +106,8 @@ void launch_gemm_f32(int epi, const GemmParams& p, hipStream_t s) {
     hipLaunchKernelGGL(gemm_f32_kernel<EPI_QKV>, grid, block, 0, s, p, tiles_n);
   else if (epi == EPI_RESID)
     hipLaunchKernelGGL(gemm_f32_kernel<EPI_RESID>, grid, block, 0, s, p, tiles_n);
+  else if (epi == EPI_STORE)
+    hipLaunchKernelGGL(gemm_f32_kernel<EPI_STORE>, grid, block, 0, s, p, tiles_n);
   else
     hipLaunchKernelGGL(gemm_f32_kernel<EPI_SWIGLU>, grid, block, 0, s, p, tiles_n);
 }

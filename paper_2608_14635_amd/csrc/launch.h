@@ -11,6 +11,7 @@ enum Epi : int {
   EPI_QKV = 0,     // RoPE on q/k; Q -> workspace, K/V -> arena slots (+ V^T for attention)
   EPI_RESID = 1,   // X += acc (fp32 residual stream)
   EPI_SWIGLU = 2,  // Hf = silu(gate) * up
+  EPI_STORE = 3,   // X = acc (fp32 output, e.g. transposed logits)
 };
 
 enum BMap : int {
@@ -94,5 +95,25 @@ constexpr int ATTN_QBLOCK_MIN = 32;
 constexpr int ROW_ALIGN = 64;  // each request's rows start on this boundary of the wave
 void launch_attention_bf16(const AttnParams& p, hipStream_t s);
 void launch_attention_f32(const AttnParams& p, int rows_total, hipStream_t s);
+
+// Resumed decode (one token per request over the paged arena).
+struct DecodeAttnParams {
+  const void* q;          // [R][nq*d] rotated queries of the step
+  const void* plane_k;    // this layer's K plane [slots][nkv][d]
+  const void* plane_v;    // this layer's V plane
+  const int32_t* tables;  // [R][max_blocks] block tables
+  int max_blocks, block_size;
+  const int32_t* ctx;     // [R] keys to attend (position + 1)
+  int nq, nkv, d;
+  int splits;             // key ranges per (request, kv head)
+  float* part;            // [R][nq][splits][d + 2] partials (o, m, l)
+  void* out;              // [R][nq*d] attention output
+};
+void launch_rope_rows(float2* table, const int32_t* positions, int rows, int d, double theta,
+                      hipStream_t s);
+int decode_attn_splits(int nkv, int64_t max_ctx);
+void launch_decode_attention(int dtype, const DecodeAttnParams& p, int num_requests, hipStream_t s);
+void launch_argmax(const float* logits_t, int64_t ld, int vocab, int num_requests,
+                   int32_t* next_tokens, float* logits_out, hipStream_t s);
 
 }  // namespace kvr

@@ -82,6 +82,32 @@ def device_model_random(shape: W.ModelShape, seed: int = 1234, device="cuda",
     return DeviceModel(shape, embed, layers, _bind_weights(shape, embed, layers))
 
 
+def device_head_from_host(shape: W.ModelShape, head: Dict, device="cuda") -> Dict[str, torch.Tensor]:
+    """Final-norm gain and LM head of the resumed decode (workloads.host_head_weights) on the device."""
+    out = {}
+    for k, a in head.items():
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        if shape.dtype == W.BF16:
+            t = t.view(torch.int16).view(torch.bfloat16)
+        out[k] = t.to(device)
+    return out
+
+
+def device_head_random(shape: W.ModelShape, seed: int = 4321, device="cuda",
+                       std: float = 0.02) -> Dict[str, torch.Tensor]:
+    """Unit final-norm gain and an N(0, std) LM head drawn on the device."""
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    dt = _TORCH_VAL[shape.dtype]
+    lm = torch.empty(shape.vocab, shape.hidden, dtype=dt, device=device)
+    flat = lm.view(-1)
+    chunk = 1 << 26
+    for i in range(0, flat.numel(), chunk):
+        n = min(chunk, flat.numel() - i)
+        flat[i:i + n] = (torch.randn(n, generator=g, device=device, dtype=torch.float32) * std).to(dt)
+    return {"final_norm": torch.ones(shape.hidden, dtype=dt, device=device), "lm_head": lm}
+
+
 def _down(model: DeviceModel, t: torch.Tensor) -> np.ndarray:
     if model.shape.dtype == W.BF16:
         return t.view(torch.int16).cpu().numpy().view(np.uint16)

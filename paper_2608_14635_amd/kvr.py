@@ -1,4 +1,5 @@
-"""Thin ctypes binding of libkvr.so (include/kvr.h, include/kvr_profile.h).
+"""Thin ctypes binding of libkvr.so (include/kvr.h, include/kvr_decode.h,
+include/kvr_profile.h).
 
 Argument marshalling only: every step of the rebuild runs in the library's
 HIP kernels.  Device buffers are passed as integer addresses (for example a
@@ -86,6 +87,14 @@ def lib() -> C.CDLL:
     L.kv_plan_release.argtypes = [vp]
     L.kv_plan_info.restype = C.c_int
     L.kv_plan_info.argtypes = [vp, C.POINTER(C.c_int32), C.POINTER(C.c_int64)]
+    L.kv_decode_workspace_bytes.restype = C.c_uint64
+    L.kv_decode_workspace_bytes.argtypes = [C.POINTER(kv_model_desc), C.c_int32, C.c_int64]
+    L.kv_decode_check.restype = C.c_int
+    L.kv_decode_check.argtypes = [C.POINTER(kv_model_desc), C.c_int32, C.c_int64, i32p, i32p,
+                                  C.c_int32, i32p, C.c_int32]
+    L.kv_decode_step.restype = C.c_int
+    L.kv_decode_step.argtypes = [C.POINTER(kv_weights), vp, vp, i32p, i32p, C.c_int32, i32p,
+                                 C.c_int32, vp, vp, C.c_uint64, vp, vp, vp]
     L.kv_profile_enable.restype = C.c_int
     L.kv_profile_enable.argtypes = [vp, C.c_int32]
     L.kv_profile_read.restype = C.c_int
@@ -201,6 +210,33 @@ def kv_plan_info(plan: int) -> Tuple[int, int]:
     return nw.value, mx.value
 
 
+def kv_decode_workspace_bytes(shape_or_desc, num_requests: int, max_position: int) -> int:
+    d = shape_or_desc if isinstance(shape_or_desc, kv_model_desc) else make_desc(shape_or_desc)
+    return int(lib().kv_decode_workspace_bytes(C.byref(d), num_requests, max_position))
+
+
+def kv_decode_check(shape_or_desc, block_size: int, num_blocks: int, tokens, positions,
+                    tables) -> int:
+    """Host-only validation of a decode step; returns the status code."""
+    d = shape_or_desc if isinstance(shape_or_desc, kv_model_desc) else make_desc(shape_or_desc)
+    tok, pos = _i32(tokens), _i32(positions)
+    tab, mb = _tables2d(tables, len(tok))
+    return int(lib().kv_decode_check(C.byref(d), block_size, num_blocks, _ptr(tok), _ptr(pos),
+                                     len(tok), _ptr(tab), mb))
+
+
+def kv_decode_step(weights: Weights, final_norm: int, lm_head: int, tokens, positions, tables,
+                   arena: int, workspace: int, workspace_bytes: int, next_tokens: int,
+                   logits: int = 0, stream: int = 0) -> None:
+    """One greedy decode step; next_tokens / logits are device addresses."""
+    tok, pos = _i32(tokens), _i32(positions)
+    tab, mb = _tables2d(tables, len(tok))
+    _check(lib().kv_decode_step(C.byref(weights.c), C.c_void_p(final_norm), C.c_void_p(lm_head),
+                                _ptr(tok), _ptr(pos), len(tok), _ptr(tab), mb, C.c_void_p(arena),
+                                C.c_void_p(workspace), workspace_bytes, C.c_void_p(stream),
+                                C.c_void_p(next_tokens), C.c_void_p(logits or None)))
+
+
 def kv_profile_enable(arena: int, enable: bool = True) -> None:
     _check(lib().kv_profile_enable(C.c_void_p(arena), 1 if enable else 0))
 
@@ -221,4 +257,4 @@ def exported_symbols() -> Iterable[str]:
     return ("kv_arena_bind", "kv_arena_release", "kv_rebuild_workspace_bytes", "kv_rebuild_check",
             "kv_rebuild", "kv_rebuild_stage", "kv_rebuild_execute", "kv_plan_release",
             "kv_plan_info", "kv_last_error", "kv_profile_enable", "kv_profile_read",
-            "kv_profile_reset")
+            "kv_profile_reset", "kv_decode_workspace_bytes", "kv_decode_check", "kv_decode_step")

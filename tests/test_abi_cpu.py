@@ -171,3 +171,75 @@ def test_unknown_handles_are_rejected(L):
     with pytest.raises(kvr.KvError) as e:
         kvr.kv_plan_release(0x1234)
     assert e.value.status == kvr.KV_ESTATE
+
+
+# ---- resumed decode: host-side checks (no device access) -----------------
+def _decode_valid(shape=W.TINY_BF16, positions=(0, 15, 40), B=16, NB=12):
+    pos = np.array(positions, np.int32)
+    toks = (np.arange(len(pos)) * 7 % shape.vocab).astype(np.int32)
+    need = pos // B + 1
+    mb = int(need.max()) + 1
+    tables = np.full((len(pos), mb), -1, np.int32)
+    nxt = 0
+    for r, n in enumerate(need):
+        tables[r, :n] = np.arange(nxt, nxt + n)
+        nxt += n
+    return shape, toks, pos, tables, B, NB
+
+
+def test_decode_workspace_bytes(L):
+    s = W.LLAMA8B
+    assert kvr.kv_decode_workspace_bytes(s, 0, 100) == 0
+    assert kvr.kv_decode_workspace_bytes(s, 4, 0) == 0
+    a = kvr.kv_decode_workspace_bytes(s, 4, 1000)
+    b = kvr.kv_decode_workspace_bytes(s, 4, 65536)
+    c = kvr.kv_decode_workspace_bytes(s, 16, 65536)
+    assert 0 < a < b < c
+    # transposed logits of the LM head: vocab x (requests padded to 256) fp32
+    assert a >= s.vocab * 256 * 4
+
+
+def test_decode_check_valid(L):
+    shape, toks, pos, tables, B, NB = _decode_valid()
+    assert kvr.kv_decode_check(shape, B, NB, toks, pos, tables) == kvr.KV_OK
+    # zero requests is a no-op
+    assert kvr.kv_decode_check(shape, B, NB, [], [], np.zeros((0, 0), np.int32)) == kvr.KV_OK
+
+
+@pytest.mark.parametrize("case,expect", [
+    ("negative_position", kvr.KV_EINVAL),
+    ("token_out_of_range", kvr.KV_ERANGE),
+    ("block_out_of_range", kvr.KV_ERANGE),
+    ("needs_more_blocks", kvr.KV_ECAPACITY),
+    ("alias_across_requests", kvr.KV_EALIAS),
+    ("alias_within_request", kvr.KV_EALIAS),
+])
+def test_decode_check_errors(L, case, expect):
+    shape, toks, pos, tables, B, NB = _decode_valid()
+    if case == "negative_position":
+        pos[1] = -1
+    elif case == "token_out_of_range":
+        toks[2] = shape.vocab
+    elif case == "block_out_of_range":
+        tables[2, 1] = NB
+    elif case == "needs_more_blocks":
+        pos[2] = B * tables.shape[1]
+    elif case == "alias_across_requests":
+        tables[2, 0] = tables[1, 0]
+    elif case == "alias_within_request":
+        tables[2, 2] = tables[2, 0]
+    assert kvr.kv_decode_check(shape, B, NB, toks, pos, tables) == expect
+
+
+def test_decode_check_ignores_unused_entries(L):
+    shape, toks, pos, tables, B, NB = _decode_valid()
+    tables[0, 1:] = 10 ** 6        # past position 0's block: never read
+    assert kvr.kv_decode_check(shape, B, NB, toks, pos, tables) == kvr.KV_OK
+
+
+def test_decode_step_rejects_unknown_arena(L):
+    shape, toks, pos, tables, B, NB = _decode_valid()
+    w = kvr.Weights(kvr.make_desc(shape), 0x1000, [{k: 0x1000 for k in kvr.LAYER_FIELDS}] * shape.num_layers)
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_decode_step(w, 0x1000, 0x1000, toks, pos, tables, 0x1234, 0x10000, 1 << 20, 0x2000)
+    assert e.value.status == kvr.KV_ESTATE
