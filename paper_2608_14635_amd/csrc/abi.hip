@@ -253,7 +253,9 @@ struct DecodeLayout {
   int32_t R = 0, npad = 0, splits = 0;
   int64_t max_position = 0;
   size_t tok = 0, pos = 0, rowidx = 0, slot = 0, ctx = 0, tables = 0, meta_end = 0;
-  size_t rope = 0, x = 0, a = 0, q = 0, u = 0, hf = 0, part = 0, logit = 0, total = 0;
+  size_t rope = 0, x = 0, a = 0, q = 0, u = 0, hf = 0, part = 0, gpart = 0, amax = 0, logit = 0;
+  size_t total = 0;
+  int64_t gpart_elems = 0;
 };
 
 DecodeLayout make_decode_layout(const kv_model_desc& d, int32_t R, int64_t max_position) {
@@ -261,7 +263,15 @@ DecodeLayout make_decode_layout(const kv_model_desc& d, int32_t R, int64_t max_p
   L.R = R;
   L.max_position = max_position;
   L.npad = (int32_t)round_up(std::max<int32_t>(R, 1), 256);
-  L.splits = decode_attn_splits(d.num_kv_heads, max_position);
+  // split counts shrink as the batch grows: size for one request's
+  L.splits = decode_attn_splits(1, d.num_kv_heads, max_position);
+  if (d.dtype == KV_BF16) {
+    const int H = d.hidden, qd = d.num_q_heads * d.head_dim, kvd = d.num_kv_heads * d.head_dim;
+    L.gpart_elems = std::max(
+        std::max(gemm_bf16_splitk_part_elems(R, qd + 2 * kvd, H), gemm_bf16_splitk_part_elems(R, H, qd)),
+        std::max(gemm_bf16_splitk_part_elems(R, 2 * d.ffn_dim, H),
+                 gemm_bf16_splitk_part_elems(R, H, d.ffn_dim)));
+  }
   const int64_t e = elem_bytes(d.dtype);
   size_t off = 0;
   auto seg = [&](size_t bytes) {
@@ -283,6 +293,8 @@ DecodeLayout make_decode_layout(const kv_model_desc& d, int32_t R, int64_t max_p
   L.u = seg((size_t)e * R * d.num_q_heads * d.head_dim);
   L.hf = seg((size_t)e * R * d.ffn_dim);
   L.part = seg((size_t)4 * R * d.num_q_heads * L.splits * (d.head_dim + 2));
+  L.gpart = seg((size_t)4 * L.gpart_elems);
+  L.amax = seg((size_t)8 * ARGMAX_CHUNKS * R);
   L.logit = seg((size_t)4 * d.vocab * L.npad);
   L.total = off;
   return L;
@@ -936,9 +948,19 @@ kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void
   void* U = ws + L.u;
   void* HF = ws + L.hf;
   float* part = reinterpret_cast<float*>(ws + L.part);
+  float* gpart = reinterpret_cast<float*>(ws + L.gpart);
+  float2* amax = reinterpret_cast<float2*>(ws + L.amax);
   float* logit_t = reinterpret_cast<float*>(ws + L.logit);
-  auto gemm = dt == KV_BF16 ? launch_gemm_bf16 : launch_gemm_f32;
   (void)e;
+  // few rows: bf16 products split K across the chip (fp32 partials summed in
+  // a fixed order); fp32 products are small enough for the plain kernel
+  auto gemm = [&](int epi, const GemmParams& gp, hipStream_t st) {
+    if (dt == KV_BF16)
+      launch_gemm_bf16_splitk(epi, gp, gpart, L.gpart_elems, st);
+    else
+      launch_gemm_f32(epi, gp, st);
+  };
+  auto gemm_full = dt == KV_BF16 ? launch_gemm_bf16 : launch_gemm_f32;
 
   // rope rows of the step's positions; the QKV epilogue indexes them by row
   launch_rope_rows(rope, d_pos, R, hd, d.rope_theta, s);
@@ -986,7 +1008,7 @@ kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void
     ap.nq = nq;
     ap.nkv = nkv;
     ap.d = hd;
-    ap.splits = L.splits;
+    ap.splits = decode_attn_splits(R, nkv, max_pos + 1);
     ap.part = part;
     ap.out = U;
     launch_decode_attention(dt, ap, R, s);
@@ -1045,8 +1067,8 @@ kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void
   gl.n_end = dt == KV_BF16 ? L.npad : R;
   gl.epi.x = logit_t;
   gl.epi.ldx = L.npad;
-  gemm(EPI_STORE, gl, s);
-  launch_argmax(logit_t, L.npad, d.vocab, R, next_tokens, logits, s);
+  gemm_full(EPI_STORE, gl, s);
+  launch_argmax(logit_t, L.npad, d.vocab, R, amax, next_tokens, logits, s);
   const hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(KV_EDEVICE, "kernel launch failed: %s", hipGetErrorString(err));
   return ok();

@@ -9,7 +9,9 @@
 // heads of that kv head.  Per block of 64 keys it stages the K and V rows in
 // LDS (coalesced 16-byte loads of whole rows), computes the g x 64 scores with
 // one key per lane (row pitch padded by 16 bytes, so 16-lane LDS phases hit
-// distinct banks), runs the online softmax per head in the exp2 domain (one
+// distinct banks; the next block is in flight in registers meanwhile, and
+// the key range's block-table entries are staged in LDS once), runs the
+// online softmax per head in the exp2 domain (one
 // wave owns a head's running max and sum), and accumulates P.V with threads
 // over (head, dim).  Each split writes (m, l, o[d]) partials; a second kernel
 // merges the splits in index order, so results do not depend on timing.
@@ -27,6 +29,7 @@ constexpr int DKB = 64;    // keys per staged block
 constexpr int DNT = 256;   // 4 waves
 constexpr int DMAXG = 16;  // q heads per kv head supported
 constexpr int DMAXD = 128;
+constexpr int TABN = 1024;  // block-table entries staged in LDS per workgroup
 
 __global__ void rope_rows_kernel(float2* table, const int32_t* positions, int rows, int half,
                                  double theta, int d) {
@@ -58,6 +61,7 @@ __global__ __launch_bounds__(DNT) void decode_attn_kernel(DecodeAttnParams p) {
   __shared__ float sq[DMAXG * DMAXD];
   __shared__ float sp[DMAXG * DKB];
   __shared__ float s_m[DMAXG], s_l[DMAXG], s_alpha[DMAXG];
+  __shared__ int s_tab[TABN];
 
   const int S = p.splits;
   int bid = blockIdx.x;
@@ -90,22 +94,50 @@ __global__ __launch_bounds__(DNT) void decode_attn_kernel(DecodeAttnParams p) {
   const int units = d * (int)sizeof(T) / 16;  // 16-byte units per row
   __syncthreads();
 
-  for (int kb = k0; kb < k1; kb += DKB) {
-    // ---- stage K and V rows of keys kb .. kb+63 (zeros past k1) ----
-    for (int i = tid; i < DKB * units; i += DNT) {
-      const int key = i / units, u = i % units;
-      const int j = kb + key;
-      uint4 kvv = make_uint4(0, 0, 0, 0), vvv = make_uint4(0, 0, 0, 0);
-      if (j < k1) {
-        const int64_t slot = (int64_t)table[j / p.block_size] * p.block_size + j % p.block_size;
-        const int64_t off = slot * row_elems + (int64_t)kvh * d;
-        kvv = reinterpret_cast<const uint4*>(Kp + off)[u];
-        vvv = reinterpret_cast<const uint4*>(Vp + off)[u];
+  // block-table entries of the key range, staged once (entries past the
+  // first TABN are read from the global table)
+  const int B = p.block_size;
+  const int b0 = k0 / B;
+  if (k0 < k1)
+    for (int i = tid; i <= (k1 - 1) / B - b0 && i < TABN; i += DNT) s_tab[i] = table[b0 + i];
+  __syncthreads();
+
+  // K/V of one 64-key block: DKB * units 16-byte pieces, PF per thread; the
+  // next block is in flight in registers while this one is used from LDS
+  // (a deeper register queue costs occupancy and was slower).
+  constexpr int PF = DKB * (DMAXD * (int)sizeof(T) / 16) / DNT;
+  uint4 ka[PF], va[PF];
+  auto fetch = [&](uint4* kr, uint4* vr, int kb) {
+#pragma unroll
+    for (int q = 0; q < PF; ++q) {
+      const int i = tid + q * DNT;
+      kr[q] = make_uint4(0, 0, 0, 0);
+      vr[q] = make_uint4(0, 0, 0, 0);
+      if (i < DKB * units) {
+        const int key = i / units, u = i % units, j = kb + key;
+        if (j < k1) {
+          const int bi = j / B - b0;
+          const int blk = bi < TABN ? s_tab[bi] : table[j / B];
+          const int64_t off = ((int64_t)blk * B + j % B) * row_elems + (int64_t)kvh * d;
+          kr[q] = reinterpret_cast<const uint4*>(Kp + off)[u];
+          vr[q] = reinterpret_cast<const uint4*>(Vp + off)[u];
+        }
       }
-      *reinterpret_cast<uint4*>(sk + key * PITCH + u * 16) = kvv;
-      *reinterpret_cast<uint4*>(sv + key * PITCH + u * 16) = vvv;
     }
-    __syncthreads();
+  };
+  auto park = [&](const uint4* kr, const uint4* vr) {
+#pragma unroll
+    for (int q = 0; q < PF; ++q) {
+      const int i = tid + q * DNT;
+      if (i < DKB * units) {
+        const int key = i / units, u = i % units;
+        *reinterpret_cast<uint4*>(sk + key * PITCH + u * 16) = kr[q];
+        *reinterpret_cast<uint4*>(sv + key * PITCH + u * 16) = vr[q];
+      }
+    }
+  };
+  // scores, online softmax and P.V of the block of keys kb.. parked in LDS
+  auto attend = [&](int kb) {
     // ---- scores: one key per lane, heads h = wid, wid+4, ... ----
     const bool kvalid = kb + lane < k1;
     for (int h = wid; h < g; h += DNT / 64) {
@@ -149,6 +181,13 @@ __global__ __launch_bounds__(DNT) void decode_attn_kernel(DecodeAttnParams p) {
       }
     }
     __syncthreads();
+  };
+  if (k0 < k1) fetch(ka, va, k0);
+  for (int kb = k0; kb < k1; kb += DKB) {
+    park(ka, va);
+    __syncthreads();
+    if (kb + DKB < k1) fetch(ka, va, kb + DKB);
+    attend(kb);
   }
 
   // ---- partials: [r][h][split][d + 2] = o[0..d), m, l ----
@@ -190,39 +229,48 @@ __global__ __launch_bounds__(DMAXD) void decode_combine_kernel(DecodeAttnParams 
   }
 }
 
-// Greedy token of request r from the transposed logits [vocab][ld]: the
-// largest value, the lowest index among equal ones; optionally the logits
-// row [r][vocab] copied out.
-__global__ __launch_bounds__(256) void argmax_kernel(const float* logits_t, int64_t ld, int vocab,
-                                                     int32_t* next_tokens, float* logits_out) {
-  __shared__ float sv[256];
-  __shared__ int si[256];
-  const int r = blockIdx.x, t = threadIdx.x;
-  float best = -INFINITY;
-  int bi = -1;
-  for (int v = t; v < vocab; v += 256) {
-    const float z = logits_t[(int64_t)v * ld + r];
-    if (logits_out) logits_out[(int64_t)r * vocab + v] = z;
-    if (bi < 0 || z > best) {
-      best = z;
-      bi = v;
-    }
-  }
-  sv[t] = best;
-  si[t] = bi;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if (t < w) {
-      const float a = sv[t], b = sv[t + w];
-      const int ia = si[t], ib = si[t + w];
-      if (ib >= 0 && (ia < 0 || b > a || (b == a && ib < ia))) {
-        sv[t] = b;
-        si[t] = ib;
+// Greedy tokens from the transposed logits [vocab][ld], in two passes.
+// Pass 1: workgroup c scans a contiguous chunk of vocabulary rows; thread t
+// follows request t (a row's requests are contiguous, so loads coalesce) and
+// keeps the largest value, the lowest index among equal ones; it also copies
+// the logits out when asked.  Pass 2 merges the chunks of each request in
+// chunk order.
+__global__ __launch_bounds__(256) void argmax_partial_kernel(const float* logits_t, int64_t ld,
+                                                             int vocab, int R, float2* partial,
+                                                             float* logits_out) {
+  const int c = blockIdx.x;
+  const int per = (vocab + ARGMAX_CHUNKS - 1) / ARGMAX_CHUNKS;
+  const int v0 = c * per, v1 = min(vocab, v0 + per);
+  for (int r = threadIdx.x; r < R; r += 256) {
+    float best = -INFINITY;
+    int bi = -1;
+    for (int v = v0; v < v1; ++v) {
+      const float z = logits_t[(int64_t)v * ld + r];
+      if (logits_out) logits_out[(int64_t)r * vocab + v] = z;
+      if (bi < 0 || z > best) {
+        best = z;
+        bi = v;
       }
     }
-    __syncthreads();
+    partial[(int64_t)c * R + r] = make_float2(best, __int_as_float(bi));
   }
-  if (t == 0) next_tokens[r] = si[0] < 0 ? 0 : si[0];
+}
+
+__global__ __launch_bounds__(64) void argmax_final_kernel(const float2* partial, int R,
+                                                          int32_t* next_tokens) {
+  const int r = blockIdx.x;
+  if (threadIdx.x != 0) return;
+  float best = -INFINITY;
+  int bi = -1;
+  for (int c = 0; c < ARGMAX_CHUNKS; ++c) {
+    const float2 e = partial[(int64_t)c * R + r];
+    const int i = __float_as_int(e.y);
+    if (i >= 0 && (bi < 0 || e.x > best)) {
+      best = e.x;
+      bi = i;
+    }
+  }
+  next_tokens[r] = bi < 0 ? 0 : bi;
 }
 
 }  // namespace
@@ -236,11 +284,13 @@ void launch_rope_rows(float2* table, const int32_t* positions, int rows, int d, 
                      positions, rows, half, theta, d);
 }
 
-int decode_attn_splits(int nkv, int64_t max_ctx) {
-  // about 1024 workgroups per request, at least 256 keys per split; independent
-  // of the request count, so a workspace sized for R requests fits any fewer
-  const int64_t want = (1024 + nkv - 1) / nkv;
-  const int64_t cap = (max_ctx + 255) / 256;
+int decode_attn_splits(int num_requests, int nkv, int64_t max_ctx) {
+  // about 2048 workgroups in all, at least 256 keys and at most 64 splits per
+  // (request, kv head); never more for more requests, so a workspace sized
+  // for one request's split count fits any larger batch
+  const int64_t pairs = std::max<int64_t>(1, (int64_t)num_requests * nkv);
+  const int64_t want = (2048 + pairs - 1) / pairs;
+  const int64_t cap = std::min<int64_t>(64, (max_ctx + 255) / 256);
   return (int)std::max<int64_t>(1, std::min(want, cap));
 }
 
@@ -259,10 +309,12 @@ void launch_decode_attention(int dtype, const DecodeAttnParams& p, int num_reque
 }
 
 void launch_argmax(const float* logits_t, int64_t ld, int vocab, int num_requests,
-                   int32_t* next_tokens, float* logits_out, hipStream_t s) {
+                   float2* partial, int32_t* next_tokens, float* logits_out, hipStream_t s) {
   if (num_requests <= 0) return;
-  hipLaunchKernelGGL(argmax_kernel, dim3(num_requests), dim3(256), 0, s, logits_t, ld, vocab,
-                     next_tokens, logits_out);
+  hipLaunchKernelGGL(argmax_partial_kernel, dim3(ARGMAX_CHUNKS), dim3(256), 0, s, logits_t, ld,
+                     vocab, num_requests, partial, logits_out);
+  hipLaunchKernelGGL(argmax_final_kernel, dim3(num_requests), dim3(64), 0, s, partial,
+                     num_requests, next_tokens);
 }
 
 }  // namespace kvr

@@ -13,6 +13,8 @@
 // an XCD share A rows and B columns in their L2.
 // Every output element is produced by exactly one workgroup with a fixed K
 // order: results are deterministic run to run.
+#include <algorithm>
+
 #include "common.h"
 #include "epilogue.h"
 #include "launch.h"
@@ -99,6 +101,7 @@ struct Loader {
   int a_voff[Ring::LOADS];
   int b_voff;
   int b_block_bytes;        // bytes between consecutive 8-row blocks of B
+  int k_base_bytes;         // first K column of this launch's K range, bytes
 };
 
 constexpr int BUF_WORD3 = 0x00020000;  // gfx9 buffer descriptor: 32-bit data format
@@ -108,7 +111,7 @@ constexpr int BUF_WORD3 = 0x00020000;  // gfx9 buffer descriptor: 32-bit data fo
 // wid+WAVES, ...).
 template <bool IS_B, int Q0, int Q1>
 __device__ __forceinline__ void issue_slot(char* smem, const Loader& L, int kt, int slot, int wid) {
-  const int kbytes = kt * BK * 2;
+  const int kbytes = L.k_base_bytes + kt * BK * 2;
   char* st = smem + (slot % Ring::NSLOT) * Ring::HALF;
 #pragma unroll
   for (int q = Q0; q < Q1; ++q) {
@@ -158,9 +161,12 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
   constexpr int SMEM = Ring::BYTES > EPI_BYTES ? Ring::BYTES : EPI_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
+  // ---- split-K pass: consecutive workgroups share a tile, one K range each ----
+  const int ksplit = EPI == EPI_PARTIAL ? p.ksplit : 1;
+  const int split = EPI == EPI_PARTIAL ? (int)(blockIdx.x % ksplit) : 0;
   // ---- tile coordinates: XCD-contiguous ranges, grouped along M ----
   const int num_tiles = tiles_m * tiles_n;
-  int t = blockIdx.x;
+  int t = EPI == EPI_PARTIAL ? (int)(blockIdx.x / ksplit) : (int)blockIdx.x;
   const int full = (num_tiles / 8) * 8;
   if (t < full) t = (t % 8) * (num_tiles / 8) + t / 8;
   const int group = t / (GROUP_M * tiles_n);
@@ -195,6 +201,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
     L.b_hi = b_row_ptr(p, tile_n, BN / 2);
     L.b_voff = (int)(lrow * ldb * 2) + unit * 16;
     L.b_block_bytes = (int)(Ring::RPB * ldb * 2);
+    L.k_base_bytes = EPI == EPI_PARTIAL ? split * p.kt_per * BK * 2 : 0;
   }
 
   f32x16 acc[FI][FJ];
@@ -205,7 +212,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int KT = p.K / BK;
+  const int KT = EPI == EPI_PARTIAL ? min(p.kt_per, p.K / BK - split * p.kt_per) : p.K / BK;
 #pragma unroll
   for (int s = 0; s < Ring::NSLOT - 2; ++s) {
     if (s & 1)
@@ -355,6 +362,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
   __syncthreads();  // all waves are done with the ring before it becomes the C tile
   float* sC = reinterpret_cast<float*>(smem);
   for (int pass = 0; pass < 2; ++pass) {
+    if (m0 + pass * 128 >= p.M) break;  // no valid rows left in this tile
     if (wm == pass) {
       // accumulator register r of tile (i, j): row 8*(r/4) + 4*(lane/32) + r%4, col lane%32
 #pragma unroll
@@ -376,6 +384,11 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
       epi_resid<BN, NT>(sC, LDC, 128, m_base, p.M, p.n_begin + tile_n * BN, p.epi);
     } else if (EPI == EPI_STORE) {
       epi_store<BN, NT>(sC, LDC, 128, m_base, p.M, p.n_begin + tile_n * BN, p.epi);
+    } else if (EPI == EPI_PARTIAL) {
+      EpiParams e = p.epi;
+      e.x = p.part + split * p.part_stride;
+      e.ldx = p.part_ld;
+      epi_store<BN, NT>(sC, LDC, 128, m_base, p.M, tile_n * BN, e);
     } else {
       epi_swiglu<bf16_t, BN, NT>(sC, LDC, 128, m_base, p.M, tile_n * (BN / 2), p.epi);
     }
@@ -383,7 +396,109 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
   }
 }
 
+// Split-K partials summed in split order into slice 0 (one float4 per
+// thread, all outputs in parallel), then the fused epilogue on slice 0 in
+// 32-row x 256-column pieces, exactly as the one-pass GEMM would apply it.
+__global__ __launch_bounds__(256) void splitk_sum_kernel(float* part, int64_t n4, int ksplit,
+                                                         int64_t stride) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n4) return;
+  float4* p0 = reinterpret_cast<float4*>(part) + i;
+  float4 a = *p0;
+  for (int sp = 1; sp < ksplit; ++sp) {
+    const float4 v = *(reinterpret_cast<const float4*>(part + sp * stride) + i);
+    a.x += v.x;
+    a.y += v.y;
+    a.z += v.z;
+    a.w += v.w;
+  }
+  *p0 = a;
+}
+
+constexpr int SK_ROWS = 32;
+template <int EPI>
+__global__ __launch_bounds__(256) void splitk_epi_kernel(GemmParams p, int tiles_n) {
+  __shared__ __attribute__((aligned(16))) float sC[SK_ROWS * LDC];
+  const int tile_n = blockIdx.x % tiles_n, m0 = (blockIdx.x / tiles_n) * SK_ROWS;
+  const int tid = threadIdx.x;
+  for (int it = tid; it < SK_ROWS * (BN / 4); it += 256) {
+    const int r = it / (BN / 4), c = (it % (BN / 4)) * 4;
+    const int m = m0 + r;
+    float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (m < p.M) a = *reinterpret_cast<const float4*>(p.part + (int64_t)m * p.part_ld + tile_n * BN + c);
+    *reinterpret_cast<float4*>(sC + r * LDC + c) = a;
+  }
+  __syncthreads();
+  if (EPI == EPI_QKV) {
+    epi_qkv<bf16_t, BN, 256>(sC, LDC, SK_ROWS, m0, p.M, p.n_begin + tile_n * BN, p.epi);
+  } else if (EPI == EPI_RESID) {
+    epi_resid<BN, 256>(sC, LDC, SK_ROWS, m0, p.M, p.n_begin + tile_n * BN, p.epi);
+  } else if (EPI == EPI_STORE) {
+    epi_store<BN, 256>(sC, LDC, SK_ROWS, m0, p.M, p.n_begin + tile_n * BN, p.epi);
+  } else {
+    epi_swiglu<bf16_t, BN, 256>(sC, LDC, SK_ROWS, m0, p.M, tile_n * (BN / 2), p.epi);
+  }
+}
+
+struct SplitPlan {
+  int tiles_m, tiles_n, ksplit, kt_per;
+};
+
+SplitPlan split_plan(int M, int N_tiles, int K) {
+  SplitPlan sp;
+  sp.tiles_m = (M + BM - 1) / BM;
+  sp.tiles_n = N_tiles;
+  const int KT = K / BK;
+  const int tiles = std::max(1, sp.tiles_m * sp.tiles_n);
+  const int want = std::max(1, std::min(KT, (256 + tiles - 1) / tiles));
+  sp.kt_per = (KT + want - 1) / want;
+  sp.ksplit = (KT + sp.kt_per - 1) / sp.kt_per;
+  return sp;
+}
+
+int n_tiles_of(const GemmParams& p) {
+  return p.bmap == BMAP_GATEUP ? p.epi.ffn / (BN / 2) : (p.n_end - p.n_begin) / BN;
+}
+
 }  // namespace
+
+int64_t gemm_bf16_splitk_part_elems(int M, int N, int K) {
+  const SplitPlan sp = split_plan(M, N / BN, K);
+  return (int64_t)sp.ksplit * M * sp.tiles_n * BN;
+}
+
+void launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s);
+
+void launch_gemm_bf16_splitk(int epi, const GemmParams& p, float* part, int64_t part_cap,
+                             hipStream_t s) {
+  if (p.M <= 0) return;
+  const SplitPlan sp = split_plan(p.M, n_tiles_of(p), p.K);
+  const int64_t ld = (int64_t)sp.tiles_n * BN;
+  if (sp.ksplit <= 1 || (int64_t)sp.ksplit * p.M * ld > part_cap) {
+    launch_gemm_bf16(epi, p, s);
+    return;
+  }
+  GemmParams q = p;
+  q.ksplit = sp.ksplit;
+  q.kt_per = sp.kt_per;
+  q.part = part;
+  q.part_ld = (int)ld;
+  q.part_stride = (int64_t)p.M * ld;
+  const dim3 grid((unsigned)(sp.tiles_m * sp.tiles_n * sp.ksplit)), block(NT);
+  hipLaunchKernelGGL(gemm_bf16_kernel<EPI_PARTIAL>, grid, block, 0, s, q, sp.tiles_m, sp.tiles_n);
+  const int64_t n4 = q.part_stride / 4;
+  hipLaunchKernelGGL(splitk_sum_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, part, n4,
+                     sp.ksplit, q.part_stride);
+  const dim3 egrid((unsigned)(((p.M + SK_ROWS - 1) / SK_ROWS) * sp.tiles_n));
+  if (epi == EPI_QKV)
+    hipLaunchKernelGGL(splitk_epi_kernel<EPI_QKV>, egrid, dim3(256), 0, s, q, sp.tiles_n);
+  else if (epi == EPI_RESID)
+    hipLaunchKernelGGL(splitk_epi_kernel<EPI_RESID>, egrid, dim3(256), 0, s, q, sp.tiles_n);
+  else if (epi == EPI_STORE)
+    hipLaunchKernelGGL(splitk_epi_kernel<EPI_STORE>, egrid, dim3(256), 0, s, q, sp.tiles_n);
+  else
+    hipLaunchKernelGGL(splitk_epi_kernel<EPI_SWIGLU>, egrid, dim3(256), 0, s, q, sp.tiles_n);
+}
 
 void launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
   const int tiles_m = (p.M + BM - 1) / BM;

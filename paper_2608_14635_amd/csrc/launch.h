@@ -12,6 +12,7 @@ enum Epi : int {
   EPI_RESID = 1,   // X += acc (fp32 residual stream)
   EPI_SWIGLU = 2,  // Hf = silu(gate) * up
   EPI_STORE = 3,   // X = acc (fp32 output, e.g. transposed logits)
+  EPI_PARTIAL = 4, // split-K pass: fp32 partial tile of one K range (see launch_gemm_bf16_splitk)
 };
 
 enum BMap : int {
@@ -53,6 +54,12 @@ struct GemmParams {
   int s0, s1;             // BMAP_QKV split points (logical columns)
   int n_begin, n_end;     // logical column range of C computed by this launch
   EpiParams epi;
+  // split-K (EPI_PARTIAL): K tiles [split*kt_per, ...) of each output tile go
+  // to part + split*part_stride, row-major with part_ld columns
+  int ksplit, kt_per;
+  float* part;
+  int64_t part_stride;
+  int part_ld;
 };
 
 // Elementwise / small kernels
@@ -66,6 +73,12 @@ int launch_probe(int* dev_flag, hipStream_t s);
 // GEMMs with fused epilogues
 void launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s);
 void launch_gemm_f32(int epi, const GemmParams& p, hipStream_t s);
+// Few-row products (the decode step): K split over enough workgroups to fill
+// the chip, fp32 partials summed in split order by a second kernel that then
+// applies the epilogue `epi`.  part holds part_cap floats.
+void launch_gemm_bf16_splitk(int epi, const GemmParams& p, float* part, int64_t part_cap,
+                             hipStream_t s);
+int64_t gemm_bf16_splitk_part_elems(int M, int N, int K);
 
 // Attention.  qblk: per q-block int4 {q_start, q_len, req_start, 0} in
 // wave-local row indices, ordered longest-first.  Each request's rows start on
@@ -111,9 +124,10 @@ struct DecodeAttnParams {
 };
 void launch_rope_rows(float2* table, const int32_t* positions, int rows, int d, double theta,
                       hipStream_t s);
-int decode_attn_splits(int nkv, int64_t max_ctx);
+int decode_attn_splits(int num_requests, int nkv, int64_t max_ctx);
 void launch_decode_attention(int dtype, const DecodeAttnParams& p, int num_requests, hipStream_t s);
+constexpr int ARGMAX_CHUNKS = 256;  // vocab chunks of the first argmax pass
 void launch_argmax(const float* logits_t, int64_t ld, int vocab, int num_requests,
-                   int32_t* next_tokens, float* logits_out, hipStream_t s);
+                   float2* partial, int32_t* next_tokens, float* logits_out, hipStream_t s);
 
 }  // namespace kvr
