@@ -35,12 +35,16 @@ class _Model(C.Structure):
     _fields_ = [("num_layers", C.c_int32), ("hidden", C.c_int32), ("num_q_heads", C.c_int32),
                 ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn_dim", C.c_int32),
                 ("vocab", C.c_int32), ("rms_eps", C.c_double), ("rope_theta", C.c_double),
-                ("dtype", C.c_int32)]
+                ("dtype", C.c_int32), ("qk_norm", C.c_int32), ("qkv_bias", C.c_int32)]
+
+
+_LAYER_KEYS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down",
+               "q_norm", "k_norm", "bq", "bk", "bv")
+_OPTIONAL = ("q_norm", "k_norm", "bq", "bk", "bv")
 
 
 class _Layer(C.Structure):
-    _fields_ = [(k, C.c_void_p) for k in ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm",
-                                          "w_gate", "w_up", "w_down")]
+    _fields_ = [(k, C.c_void_p) for k in _LAYER_KEYS]
 
 
 class _Arena(C.Structure):
@@ -85,7 +89,8 @@ class Oracle:
         return _Model(num_layers if num_layers is not None else shape.num_layers, shape.hidden,
                       shape.num_q_heads, shape.num_kv_heads, shape.head_dim, shape.ffn_dim,
                       shape.vocab, float(shape.rms_eps), float(shape.rope_theta),
-                      shape.dtype if dtype is None else dtype)
+                      shape.dtype if dtype is None else dtype,
+                      int(getattr(shape, "qk_norm", False)), int(getattr(shape, "qkv_bias", False)))
 
     @staticmethod
     def _check(a: np.ndarray, dt: int) -> np.ndarray:
@@ -95,8 +100,10 @@ class Oracle:
     def _layers(self, weights: Dict, dt: int):
         arr = (_Layer * len(weights["layers"]))()
         for i, lw in enumerate(weights["layers"]):
-            for k in _Layer._fields_:
-                setattr(arr[i], k[0], self._check(lw[k[0]], dt).ctypes.data)
+            for k, _ in _Layer._fields_:
+                if k in _OPTIONAL and k not in lw:
+                    continue
+                setattr(arr[i], k, self._check(lw[k], dt).ctypes.data)
         return arr
 
     @staticmethod

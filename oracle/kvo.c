@@ -121,6 +121,34 @@ static void project(const void* W, int dt, int64_t N, int64_t K, const double* A
   }
 }
 
+/* out[r][i] = to_work(W[i] . A[r] + b[i]): the bias joins the sum before the
+ * single rounding */
+static void project_bias(const void* W, const void* b, int dt, int64_t N, int64_t K,
+                         const double* A, int64_t cnt, double* out) {
+  int64_t idx;
+#pragma omp parallel for schedule(static)
+  for (idx = 0; idx < cnt * N; ++idx) {
+    int64_t r = idx / N, i = idx % N;
+    out[idx] = to_work(dot_row(W, dt, i, K, A + r * K) + load(b, dt, i), dt);
+  }
+}
+
+/* per-head RMSNorm with a gain over the head dims, in place on [cnt][nh][d];
+ * the result stays in working precision (RoPE and the rounding follow) */
+static void head_rmsnorm(double* u, const void* g, int dt, int64_t cnt, int64_t nh, int64_t d,
+                         double eps) {
+  int64_t idx;
+#pragma omp parallel for schedule(static)
+  for (idx = 0; idx < cnt * nh; ++idx) {
+    double* hu = u + idx * d;
+    double ss = 0.0, inv;
+    int64_t e;
+    for (e = 0; e < d; ++e) ss += hu[e] * hu[e];
+    inv = 1.0 / sqrt(ss / (double)d + eps);
+    for (e = 0; e < d; ++e) hu[e] = to_work(load(g, dt, e) * hu[e] * inv, dt);
+  }
+}
+
 /* RMSNorm with gain, one rounding at the end */
 static void rmsnorm(const double* x, const void* g, int dt, int64_t H, double eps,
                     int64_t cnt, double* out) {
@@ -177,9 +205,19 @@ static void layer_step(const kvo_model* m, const kvo_layer* lw, int l, double* x
 
   /* attention RMSNorm and Q/K/V projections */
   rmsnorm(x, lw->attn_norm, dt, H, m->rms_eps, cnt, a);
-  project(lw->wq, dt, nq * d, H, a, cnt, q);
-  project(lw->wk, dt, nkv * d, H, a, cnt, k);
-  project(lw->wv, dt, nkv * d, H, a, cnt, v);
+  if (m->qkv_bias) {
+    project_bias(lw->wq, lw->bq, dt, nq * d, H, a, cnt, q);
+    project_bias(lw->wk, lw->bk, dt, nkv * d, H, a, cnt, k);
+    project_bias(lw->wv, lw->bv, dt, nkv * d, H, a, cnt, v);
+  } else {
+    project(lw->wq, dt, nq * d, H, a, cnt, q);
+    project(lw->wk, dt, nkv * d, H, a, cnt, k);
+    project(lw->wv, dt, nkv * d, H, a, cnt, v);
+  }
+  if (m->qk_norm) {
+    head_rmsnorm(q, lw->q_norm, dt, cnt, nq, d, m->rms_eps);
+    head_rmsnorm(k, lw->k_norm, dt, cnt, nkv, d, m->rms_eps);
+  }
 
   /* RoPE on q and k, round, write K^ / V^ to the arena */
 #pragma omp parallel for schedule(static)

@@ -14,7 +14,9 @@
  * Finding 2).  The paper does not write out the model forward; the oracle
  * takes a Llama-style pre-norm decoder (RMSNorm, Q/K/V projections, NeoX
  * half-split RoPE, causal GQA softmax attention, output projection, SwiGLU
- * FFN, fp32 residual stream) and writes the rotated K and the V of every
+ * FFN, fp32 residual stream), optionally with the two variants of the Qwen
+ * models the paper evaluates (Sec. 7.1; Fig. 3 uses Qwen2.5): biases on the
+ * q/k/v projections, and a per-head RMSNorm of q and k before RoPE and writes the rotated K and the V of every
  * position of every layer into a paged arena through per-request block tables.
  *
  * Precision contract: every reduction is accumulated in fp64; every op output
@@ -37,11 +39,16 @@ typedef struct {
   int32_t num_layers, hidden, num_q_heads, num_kv_heads, head_dim, ffn_dim, vocab;
   double rms_eps, rope_theta;
   int32_t dtype;         /* element type of weights and arena: KVO_F32/BF16/F64 */
+  int32_t qk_norm;       /* 1: per-head RMSNorm of q and k before RoPE (Qwen3)   */
+  int32_t qkv_bias;      /* 1: q, k, v projections carry a bias (Qwen2.5)        */
 } kvo_model;
 
-/* One layer's weights, host pointers, nn.Linear layout [out, in] row-major. */
+/* One layer's weights, host pointers, nn.Linear layout [out, in] row-major.
+ * q_norm, k_norm [head_dim] (qk_norm models); bq [nq*d], bk, bv [nkv*d]
+ * (qkv_bias models); otherwise NULL. */
 typedef struct {
   const void *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *w_gate, *w_up, *w_down;
+  const void *q_norm, *k_norm, *bq, *bk, *bv;
 } kvo_layer;
 
 /* Paged arena (host memory): element offset of (layer l, plane kv, block b,

@@ -46,6 +46,8 @@ class ModelShape:
     rms_eps: float
     rope_theta: float
     dtype: int
+    qk_norm: bool = False    # per-head RMSNorm of q and k before RoPE (Qwen3)
+    qkv_bias: bool = False   # biases on the q, k, v projections (Qwen2.5)
 
     @property
     def elem_bytes(self) -> int:
@@ -77,6 +79,11 @@ QWEN32B = ModelShape(64, 5120, 40, 8, 128, 27648, 152064, 1e-6, 1e6, BF16)
 # small bf16 decoder used by fast parity tests: several MFMA tiles per GEMM,
 # GQA group 4, head_dim 128 like the real shapes.
 TINY_BF16 = ModelShape(4, 512, 8, 2, 128, 1408, 1000, 1e-5, 1e4, BF16)
+# The paper's own model families (Sec. 7.1 evaluates Qwen3 4B-32B; Fig. 3 uses
+# Qwen2.5-1.5B): public decoder shapes with their attention variants.
+QWEN3_8B = ModelShape(36, 4096, 32, 8, 128, 12288, 151936, 1e-6, 1e6, BF16, qk_norm=True)
+QWEN3_32B = ModelShape(64, 5120, 64, 8, 128, 25600, 151936, 1e-6, 1e6, BF16, qk_norm=True)
+QWEN25_1_5B = ModelShape(28, 1536, 12, 2, 128, 8960, 151936, 1e-6, 1e6, BF16, qkv_bias=True)
 
 SHAPES = {"tiny_f32": TINY_F32, "llama8b": LLAMA8B, "qwen14b": QWEN14B,
           "qwen32b": QWEN32B, "tiny_bf16": TINY_BF16}
@@ -262,10 +269,18 @@ LAYER_KEYS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up",
 
 
 def layer_shapes(s: ModelShape) -> Dict[str, tuple]:
+    """Per-layer weight shapes; the variant weights come after the common ones,
+    so turning a variant on leaves the draws of the common weights unchanged."""
     H, d = s.hidden, s.head_dim
-    return {"attn_norm": (H,), "wq": (s.num_q_heads * d, H), "wk": (s.num_kv_heads * d, H),
-            "wv": (s.num_kv_heads * d, H), "wo": (H, s.num_q_heads * d), "ffn_norm": (H,),
-            "w_gate": (s.ffn_dim, H), "w_up": (s.ffn_dim, H), "w_down": (H, s.ffn_dim)}
+    out = {"attn_norm": (H,), "wq": (s.num_q_heads * d, H), "wk": (s.num_kv_heads * d, H),
+           "wv": (s.num_kv_heads * d, H), "wo": (H, s.num_q_heads * d), "ffn_norm": (H,),
+           "w_gate": (s.ffn_dim, H), "w_up": (s.ffn_dim, H), "w_down": (H, s.ffn_dim)}
+    if s.qk_norm:
+        out.update({"q_norm": (d,), "k_norm": (d,)})
+    if s.qkv_bias:
+        out.update({"bq": (s.num_q_heads * d,), "bk": (s.num_kv_heads * d,),
+                    "bv": (s.num_kv_heads * d,)})
+    return out
 
 
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:

@@ -408,6 +408,68 @@ def pin_empty_and_single(o):
 
 
 # ----------------------------------------------------------------------
+# the Qwen attention variants: per-head q/k RMSNorm (Qwen3), q/k/v bias (Qwen2.5)
+# ----------------------------------------------------------------------
+VARIANTS = {"qk_norm": dict(qk_norm=True), "qkv_bias": dict(qkv_bias=True),
+            "both": dict(qk_norm=True, qkv_bias=True)}
+
+
+def pin_torch_variants_f64(o):
+    for name, kw in VARIANTS.items():
+        base = dataclasses.replace(TINY_GQA, **kw)
+        shape = dataclasses.replace(base, dtype=F64)
+        wl = W.small_workload(base, [5, 19, 1], seed=150, other_live_frac=0.0)
+        w = weights_in(W.host_weights(base, seed=51), F32, F64)
+        _torch_compare(o, shape, dataclasses.replace(wl, shape=shape), w, F64, None, 1e-10)
+
+
+def pin_torch_variants_rounding(o):
+    for name, kw in VARIANTS.items():
+        for base, rounding, tol in ((dataclasses.replace(TINY_GQA, **kw), "f32", 1e-5),
+                                    (dataclasses.replace(TINY_BF16_2L, **kw), "bf16", 2e-2)):
+            wl = W.small_workload(base, [5, 19], seed=151, other_live_frac=0.0)
+            w = W.host_weights(base, seed=52)
+            _torch_compare(o, base, wl, w, base.dtype, rounding, tol)
+
+
+def pin_qk_norm_scale_invariance(o):
+    """With the per-head norm (and eps = 0) q and k do not depend on the scale
+    of Wq and Wk: scaling both by 3 leaves every K/V output unchanged up to
+    fp64 rounding, while it does change them without the norm."""
+    for qk in (True, False):
+        shape = dataclasses.replace(TINY_GQA, dtype=F64, qk_norm=qk, rms_eps=0.0)
+        wl = W.small_workload(shape, [7, 12], seed=152, other_live_frac=0.0)
+        w = weights_in(W.host_weights(dataclasses.replace(shape, dtype=F32), seed=53), F32, F64)
+        w3 = {"embed": w["embed"], "layers": [dict(lw) for lw in w["layers"]]}
+        for lw in w3["layers"]:
+            lw["wq"] = lw["wq"] * 3.0
+            lw["wk"] = lw["wk"] * 3.0
+        a1 = run(o, shape, w, wl, dt=F64)
+        a3 = run(o, shape, w3, wl, dt=F64)
+        err = normwise(a3[np.isfinite(a3)], a1[np.isfinite(a1)])
+        if qk:
+            assert err < 1e-12, err
+        else:
+            assert err > 1e-3, err
+
+
+def pin_value_bias_closed_form(o):
+    """With Wv = 0 every value row is the bias: V of every layer equals
+    rnd(bv) at every position, and attention returns exactly that row."""
+    shape = dataclasses.replace(TINY_BF16_2L, qkv_bias=True)
+    wl = W.small_workload(shape, [3, 17], seed=153, other_live_frac=0.0)
+    w = W.host_weights(shape, seed=54)
+    for lw in w["layers"]:
+        lw["wv"] = np.zeros_like(lw["wv"])
+    a = run(o, shape, w, wl)
+    for r in range(wl.num_requests):
+        _, V = gather(wl, shape, a, r)
+        for l in range(shape.num_layers):
+            bv = w["layers"][l]["bv"].reshape(shape.num_kv_heads, shape.head_dim)
+            assert np.array_equal(V[l], np.broadcast_to(bv, V[l].shape))
+
+
+# ----------------------------------------------------------------------
 # resumed decode (the step after the rebuild): final norm, LM head, greedy
 # ----------------------------------------------------------------------
 def _head_in(head: dict, src_dt: int, dst_dt: int) -> dict:

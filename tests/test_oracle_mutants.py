@@ -44,6 +44,14 @@ MUTANTS = [
      "layer_step(m, &layers[l], l, x, positions[r] + 1, 1, table, arena, kv_only, scratch);", 0),
     ("decode_step_first_table", "const int32_t* table = block_tables + (int64_t)r * max_blocks;",
      "const int32_t* table = block_tables;", 2),
+    ("q_norm_skipped", "head_rmsnorm(q, lw->q_norm, dt, cnt, nq, d, m->rms_eps);", ";", 0),
+    ("q_norm_with_k_gain", "head_rmsnorm(q, lw->q_norm, dt, cnt, nq, d, m->rms_eps);",
+     "head_rmsnorm(q, lw->k_norm, dt, cnt, nq, d, m->rms_eps);", 0),
+    ("head_norm_sum_not_mean", "inv = 1.0 / sqrt(ss / (double)d + eps);", "inv = 1.0 / sqrt(ss + eps);", 0),
+    ("bias_dropped", "to_work(dot_row(W, dt, i, K, A + r * K) + load(b, dt, i), dt)",
+     "to_work(dot_row(W, dt, i, K, A + r * K), dt)", 0),
+    ("v_bias_from_k", "project_bias(lw->wv, lw->bv, dt, nkv * d, H, a, cnt, v);",
+     "project_bias(lw->wv, lw->bk, dt, nkv * d, H, a, cnt, v);", 0),
 ]
 
 

@@ -62,9 +62,12 @@ def forward(shape: W.ModelShape, w64: Dict, tokens: np.ndarray,
     Ks, Vs = [], []
     for lw in w64["layers"]:
         a = rnd(F.rms_norm(x, (H,), weight=lw["attn_norm"], eps=float(shape.rms_eps)))
-        q = work(F.linear(a, lw["wq"])).view(n, nq, d)
-        k = work(F.linear(a, lw["wk"])).view(n, nkv, d)
-        v = work(F.linear(a, lw["wv"])).view(n, nkv, d)
+        q = work(F.linear(a, lw["wq"], lw.get("bq"))).view(n, nq, d)
+        k = work(F.linear(a, lw["wk"], lw.get("bk"))).view(n, nkv, d)
+        v = work(F.linear(a, lw["wv"], lw.get("bv"))).view(n, nkv, d)
+        if getattr(shape, "qk_norm", False):
+            q = work(F.rms_norm(q, (d,), weight=lw["q_norm"], eps=float(shape.rms_eps)))
+            k = work(F.rms_norm(k, (d,), weight=lw["k_norm"], eps=float(shape.rms_eps)))
         q = rnd(work(q * cos + _rotate_half(q) * sin))
         k = rnd(work(k * cos + _rotate_half(k) * sin))
         v = rnd(v)
