@@ -183,6 +183,9 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--model", default="",
+                    help="run the configuration's request mix on another decoder shape "
+                         "(e.g. qwen3_8b, qwen3_32b, qwen25_1_5b: the paper's model families)")
     ap.add_argument("--wave-tokens", type=int, default=0, help="0 = largest that fits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
@@ -213,6 +216,8 @@ def main():
     torch.cuda.set_device(0)
     cfg = args.config
     shape = {1: W.TINY_F32, 2: W.LLAMA8B, 3: W.LLAMA8B, 4: W.QWEN14B, 5: W.QWEN32B}[cfg]
+    if args.model:
+        shape = W.SHAPES[args.model]
     log = lambda m: print(m, file=sys.stderr, flush=True)  # noqa: E731
 
     log(f"[bench] config {cfg}: generating weights on the device")
@@ -220,15 +225,15 @@ def main():
     torch.cuda.synchronize()
     if cfg in (3, 5):
         # arena fills the HBM left after weights and workspace (2 GiB margin)
-        probe = W.CONFIGS[cfg](num_blocks=1 << 30)
+        probe = W.CONFIGS[cfg](num_blocks=1 << 30, shape=shape)
         wave = args.wave_tokens or min(probe.total_tokens, 131072)
         ws_bytes = kvr.kv_rebuild_workspace_bytes(shape, probe.num_requests, probe.total_tokens, wave)
         free, _ = torch.cuda.mem_get_info()
         per_block = shape.num_layers * 2 * 16 * shape.kv_row_elems() * shape.elem_bytes
         nb = int((free - ws_bytes - (2 << 30)) // per_block)
-        wl = W.CONFIGS[cfg](num_blocks=nb)
+        wl = W.CONFIGS[cfg](num_blocks=nb, shape=shape)
     else:
-        wl = W.CONFIGS[cfg]()
+        wl = W.CONFIGS[cfg](shape=shape) if cfg != 1 else W.CONFIGS[cfg]()
     T = wl.total_tokens
     wave = args.wave_tokens or min(T, 131072 if cfg != 5 else 65536)
     log(f"[bench] R={wl.num_requests} T={T} NB={wl.num_blocks} arena={wl.arena_bytes() / 2**30:.1f} GiB")
@@ -308,7 +313,8 @@ def main():
         "value": T / sec, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_wall, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": dt_name, "data": "synthetic",
-        "config": {"workload": wl.name, "requests": wl.num_requests, "total_tokens": T,
+        "config": {"workload": wl.name + (f"@{args.model}" if args.model else ""),
+                   "requests": wl.num_requests, "total_tokens": T,
                    "block_size": wl.block_size, "num_blocks": wl.num_blocks,
                    "layers": shape.num_layers, "hidden": shape.hidden,
                    "heads": f"{shape.num_q_heads}/{shape.num_kv_heads}x{shape.head_dim}",

@@ -56,20 +56,29 @@ typedef enum { KV_F32 = 0, KV_BF16 = 1 } kv_dtype;
 /* Decoder shape.  Weights, activations and arena share `dtype`.
  * Supported: num_q_heads % num_kv_heads == 0; for KV_BF16 head_dim == 128,
  * hidden % 256 == 0, num_kv_heads even, ffn_dim % 128 == 0; for KV_F32
- * 128 % head_dim == 0 and (num_kv_heads * head_dim) % 128 == 0. */
+ * 128 % head_dim == 0 and (num_kv_heads * head_dim) % 128 == 0.
+ * Two attention variants of the model families the paper evaluates (Qwen3
+ * in Sec. 7.1, Qwen2.5 in Fig. 3): qk_norm = 1 applies an RMSNorm with a
+ * [head_dim] gain (and rms_eps) to every q and k head before RoPE (head_dim
+ * >= 32); qkv_bias = 1 adds biases to the q, k and v projections. */
 typedef struct {
   int32_t num_layers, hidden, num_q_heads, num_kv_heads, head_dim, ffn_dim, vocab;
   double rms_eps;    /* RMSNorm epsilon                                   */
   double rope_theta; /* RoPE base; angle of pair i at position p is p * theta^(-2i/d) */
   int32_t dtype;     /* kv_dtype                                          */
+  int32_t qk_norm;   /* 0 or 1: per-head q/k RMSNorm before RoPE          */
+  int32_t qkv_bias;  /* 0 or 1: biases on the q, k, v projections         */
 } kv_model_desc;
 
 /* One layer, device pointers, nn.Linear layout [out, in] row-major:
  * attn_norm, ffn_norm [hidden]; wq [nq*d, hidden]; wk, wv [nkv*d, hidden]
  * (row h*d + e is head h, dim e); wo [hidden, nq*d]; w_gate, w_up
- * [ffn, hidden]; w_down [hidden, ffn].  Read in place, never copied. */
+ * [ffn, hidden]; w_down [hidden, ffn].  Variant weights: q_norm, k_norm
+ * [head_dim] (required when qk_norm), bq [nq*d], bk, bv [nkv*d] (required
+ * when qkv_bias); NULL otherwise.  Read in place, never copied. */
 typedef struct {
   const void *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *w_gate, *w_up, *w_down;
+  const void *q_norm, *k_norm, *bq, *bk, *bv;
 } kv_layer_weights;
 
 typedef struct {

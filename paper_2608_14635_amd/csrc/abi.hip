@@ -54,6 +54,9 @@ kv_status check_desc(const kv_model_desc* d) {
     return fail(KV_EINVAL, "num_q_heads must be a multiple of num_kv_heads");
   if (d->hidden % 8 != 0 || d->hidden > 8192)
     return fail(KV_EINVAL, "hidden must be a multiple of 8 and at most 8192");
+  if ((d->qk_norm != 0 && d->qk_norm != 1) || (d->qkv_bias != 0 && d->qkv_bias != 1))
+    return fail(KV_EINVAL, "qk_norm and qkv_bias must be 0 or 1");
+  if (d->qk_norm && d->head_dim < 32) return fail(KV_EINVAL, "qk_norm needs head_dim >= 32");
   if (d->dtype == KV_BF16) {
     if (d->head_dim != 128) return fail(KV_EINVAL, "bf16 models need head_dim == 128");
     if (d->hidden % 256 != 0) return fail(KV_EINVAL, "bf16 models need hidden % 256 == 0");
@@ -76,7 +79,7 @@ bool same_desc(const kv_model_desc& a, const kv_model_desc& b) {
   return a.num_layers == b.num_layers && a.hidden == b.hidden && a.num_q_heads == b.num_q_heads &&
          a.num_kv_heads == b.num_kv_heads && a.head_dim == b.head_dim && a.ffn_dim == b.ffn_dim &&
          a.vocab == b.vocab && a.rms_eps == b.rms_eps && a.rope_theta == b.rope_theta &&
-         a.dtype == b.dtype;
+         a.dtype == b.dtype && a.qk_norm == b.qk_norm && a.qkv_bias == b.qkv_bias;
 }
 
 // ---------------------------------------------------------------------------
@@ -651,6 +654,10 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
     if (!lw.attn_norm || !lw.wq || !lw.wk || !lw.wv || !lw.wo || !lw.ffn_norm || !lw.w_gate ||
         !lw.w_up || !lw.w_down)
       return fail(KV_EINVAL, "null weight pointer in layer %d", l);
+    if (d.qk_norm && (!lw.q_norm || !lw.k_norm))
+      return fail(KV_EINVAL, "qk_norm model without q_norm/k_norm in layer %d", l);
+    if (d.qkv_bias && (!lw.bq || !lw.bk || !lw.bv))
+      return fail(KV_EINVAL, "qkv_bias model without bq/bk/bv in layer %d", l);
   }
   if (plan->waves.empty()) return ok();
   DeviceGuard dg(ar->device);
@@ -727,6 +734,12 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
       g.epi.nq = nq;
       g.epi.nkv = nkv;
       g.epi.d = hd;
+      g.epi.bq = d.qkv_bias ? lw.bq : nullptr;
+      g.epi.bk = d.qkv_bias ? lw.bk : nullptr;
+      g.epi.bv = d.qkv_bias ? lw.bv : nullptr;
+      g.epi.q_norm = d.qk_norm ? lw.q_norm : nullptr;
+      g.epi.k_norm = d.qk_norm ? lw.k_norm : nullptr;
+      g.epi.eps = eps;
       {
         ProfScope ps(ar, s, KV_PROF_GEMM_QKV, 2.0 * wv.tokens * (double)(g.n_end - g.n_begin) * H);
         gemm(EPI_QKV, g, s);
@@ -869,6 +882,10 @@ kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void
     if (!lw.attn_norm || !lw.wq || !lw.wk || !lw.wv || !lw.wo || !lw.ffn_norm || !lw.w_gate ||
         !lw.w_up || !lw.w_down)
       return fail(KV_EINVAL, "null weight pointer in layer %d", l);
+    if (d.qk_norm && (!lw.q_norm || !lw.k_norm))
+      return fail(KV_EINVAL, "qk_norm model without q_norm/k_norm in layer %d", l);
+    if (d.qkv_bias && (!lw.bq || !lw.bk || !lw.bv))
+      return fail(KV_EINVAL, "qkv_bias model without bq/bk/bv in layer %d", l);
   }
   if (!workspace) return fail(KV_EINVAL, "null workspace");
   const DecodeLayout L = make_decode_layout(d, R, max_pos + 1);
@@ -995,6 +1012,12 @@ kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void
     g.epi.nq = nq;
     g.epi.nkv = nkv;
     g.epi.d = hd;
+    g.epi.bq = d.qkv_bias ? lw.bq : nullptr;
+    g.epi.bk = d.qkv_bias ? lw.bk : nullptr;
+    g.epi.bv = d.qkv_bias ? lw.bv : nullptr;
+    g.epi.q_norm = d.qk_norm ? lw.q_norm : nullptr;
+    g.epi.k_norm = d.qk_norm ? lw.k_norm : nullptr;
+    g.epi.eps = eps;
     gemm(EPI_QKV, g, s);
 
     DecodeAttnParams ap{};

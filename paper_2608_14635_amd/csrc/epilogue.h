@@ -18,16 +18,53 @@ namespace kvr {
 
 // QKV: the tile covers logical columns [n0, n0+BN) lying in one region
 // (q: [0, nq*d), k: [nq*d, nq*d + nkv*d), v: after that) and BN % d == 0.
+// Variants: biases are added to the accumulators first; with per-head q/k
+// norms, a first pass writes each (row, head)'s inverse RMS into the spare
+// columns BN.. of the parked tile (ldc >= BN + BN/d), then the rotary pass
+// scales by it and by the gain.
 template <typename T, int BN, int NT>
-__device__ __forceinline__ void epi_qkv(const float* sC, int ldc, int rows, int m_base, int M,
+__device__ __forceinline__ void epi_qkv(float* sC, int ldc, int rows, int m_base, int M,
                                         int n0, const EpiParams& e) {
   const int tid = threadIdx.x;
   const int d = e.d, half = d >> 1;
   const int qcols = e.nq * d, kcols = e.nkv * d;
   const int region = n0 < qcols ? 0 : (n0 < qcols + kcols ? 1 : 2);
   if (region < 2) {
-    // items: (row, head in tile, chunk of 8 rotary pairs)
+    // column base of the tile within its region (q: head-major q columns,
+    // k: head-major k columns), bias and norm gain of the region
+    const int rbase = region == 0 ? n0 : n0 - qcols;
+    const T* bias = reinterpret_cast<const T*>(region == 0 ? e.bq : e.bk);
+    const T* gain = reinterpret_cast<const T*>(region == 0 ? e.q_norm : e.k_norm);
     const int heads = BN / d, chunks = half / 8;
+    if (gain != nullptr) {
+      // eight consecutive lanes per (row, head), each summing d/8 squares
+      const int seg = d / 8;
+      for (int it = tid; it < rows * heads * 8; it += NT) {
+        const int pr = it >> 3, part = it & 7;
+        const int r = pr / heads, hh = pr % heads;
+        const float* src = sC + (int64_t)r * ldc + hh * d + part * seg;
+        const int bb = rbase + hh * d + part * seg;
+        float ss = 0.0f;
+        for (int i = 0; i < seg; i += 4) {
+          float b4[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+          if (bias) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) b4[k] = Elem<T>::load(bias, bb + i + k);
+          }
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const float v = src[i + k] + b4[k];
+            ss += v * v;
+          }
+        }
+        ss += __shfl_xor(ss, 1, 64);
+        ss += __shfl_xor(ss, 2, 64);
+        ss += __shfl_xor(ss, 4, 64);
+        if (part == 0) sC[(int64_t)r * ldc + BN + hh] = 1.0f / sqrtf(ss / (float)d + e.eps);
+      }
+      __syncthreads();
+    }
+    // items: (row, head in tile, chunk of 8 rotary pairs)
     const int per_row = heads * chunks;
     for (int it = tid; it < rows * per_row; it += NT) {
       const int r = it / per_row, hc = it % per_row;
@@ -37,10 +74,28 @@ __device__ __forceinline__ void epi_qkv(const float* sC, int ldc, int rows, int 
       const float* src = sC + (int64_t)r * ldc + hh * d;
       const int p = e.pos[m];
       const float2* cs = e.rope + (int64_t)p * half + c0;
-      float lo[8], hi[8];
+      const int hb = rbase + hh * d;
+      const float inv = gain != nullptr ? sC[(int64_t)r * ldc + BN + hh] : 1.0f;
+      float lo[8], hi[8], ba[8], bb[8], ga[8], gb[8];
+      if (bias) {
+        ld8(bias + hb + c0, ba);
+        ld8(bias + hb + c0 + half, bb);
+      }
+      if (gain != nullptr) {
+        ld8(gain + c0, ga);
+        ld8(gain + c0 + half, gb);
+      }
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const float a = src[c0 + i], b = src[c0 + half + i];
+        float a = src[c0 + i], b = src[c0 + half + i];
+        if (bias) {
+          a += ba[i];
+          b += bb[i];
+        }
+        if (gain != nullptr) {
+          a = a * inv * ga[i];
+          b = b * inv * gb[i];
+        }
         const float2 t = cs[i];
         lo[i] = Elem<T>::round(a * t.x - b * t.y);
         hi[i] = Elem<T>::round(b * t.x + a * t.y);
@@ -70,6 +125,15 @@ __device__ __forceinline__ void epi_qkv(const float* sC, int ldc, int rows, int 
     }
   } else {
     const int vbase = n0 - qcols - kcols;  // first V column (head-major) of the tile
+    const T* bias = reinterpret_cast<const T*>(e.bv);
+    if (bias != nullptr) {
+      // fold the bias into the parked tile once; both stores below read it
+      for (int it = tid; it < rows * BN; it += NT) {
+        const int r = it / BN, c = it % BN;
+        sC[(int64_t)r * ldc + c] += Elem<T>::load(bias, vbase + c);
+      }
+      __syncthreads();
+    }
     const int per_row = BN / 8;
     for (int it = tid; it < rows * per_row; it += NT) {
       const int r = it / per_row, c0 = (it % per_row) * 8;

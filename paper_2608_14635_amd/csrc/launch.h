@@ -33,6 +33,13 @@ struct EpiParams {
   const int32_t* pos;     // per wave-local token: position within its request
   const float2* rope;     // [max_pos][d/2] (cos, sin)
   int nq, nkv, d;
+  // QKV variants: q/k/v biases (null = none) and per-head q/k RMSNorm gains
+  const void* bq;
+  const void* bk;
+  const void* bv;
+  const void* q_norm;     // null = no per-head norm
+  const void* k_norm;
+  float eps;
   // RESID
   float* x;               // [rows][ldx]
   int ldx;

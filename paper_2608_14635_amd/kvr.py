@@ -24,7 +24,9 @@ STATUS_NAMES = {0: "KV_OK", -1: "KV_EINVAL", -2: "KV_ERANGE", -3: "KV_EALIAS", -
                 -5: "KV_EDEVICE", -6: "KV_ENOMEM", -7: "KV_ESTATE"}
 KV_F32, KV_BF16 = 0, 1
 PROF_CLASSES = ("rope", "norm", "gemm_qkv", "attention", "gemm_o", "gemm_gateup", "gemm_down")
-LAYER_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
+LAYER_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down",
+                "q_norm", "k_norm", "bq", "bk", "bv")
+OPTIONAL_FIELDS = ("q_norm", "k_norm", "bq", "bk", "bv")
 
 
 class KvError(RuntimeError):
@@ -38,7 +40,7 @@ class kv_model_desc(C.Structure):
     _fields_ = [("num_layers", C.c_int32), ("hidden", C.c_int32), ("num_q_heads", C.c_int32),
                 ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn_dim", C.c_int32),
                 ("vocab", C.c_int32), ("rms_eps", C.c_double), ("rope_theta", C.c_double),
-                ("dtype", C.c_int32)]
+                ("dtype", C.c_int32), ("qk_norm", C.c_int32), ("qkv_bias", C.c_int32)]
 
 
 class kv_layer_weights(C.Structure):
@@ -127,7 +129,8 @@ def make_desc(shape) -> kv_model_desc:
     """kv_model_desc from any object with the ModelShape fields."""
     return kv_model_desc(shape.num_layers, shape.hidden, shape.num_q_heads, shape.num_kv_heads,
                          shape.head_dim, shape.ffn_dim, shape.vocab, float(shape.rms_eps),
-                         float(shape.rope_theta), int(shape.dtype))
+                         float(shape.rope_theta), int(shape.dtype),
+                         int(getattr(shape, "qk_norm", False)), int(getattr(shape, "qkv_bias", False)))
 
 
 class Weights:
@@ -137,6 +140,8 @@ class Weights:
         self._layers = (kv_layer_weights * len(layer_ptrs))()
         for i, lp in enumerate(layer_ptrs):
             for k in LAYER_FIELDS:
+                if k in OPTIONAL_FIELDS and k not in lp:
+                    continue
                 setattr(self._layers[i], k, lp[k])
         self.c = kv_weights(desc, embed_ptr, C.cast(self._layers, C.POINTER(kv_layer_weights)))
 

@@ -86,7 +86,8 @@ QWEN3_32B = ModelShape(64, 5120, 64, 8, 128, 25600, 151936, 1e-6, 1e6, BF16, qk_
 QWEN25_1_5B = ModelShape(28, 1536, 12, 2, 128, 8960, 151936, 1e-6, 1e6, BF16, qkv_bias=True)
 
 SHAPES = {"tiny_f32": TINY_F32, "llama8b": LLAMA8B, "qwen14b": QWEN14B,
-          "qwen32b": QWEN32B, "tiny_bf16": TINY_BF16}
+          "qwen32b": QWEN32B, "tiny_bf16": TINY_BF16, "qwen3_8b": QWEN3_8B,
+          "qwen3_32b": QWEN3_32B, "qwen25_1_5b": QWEN25_1_5B}
 
 
 @dataclasses.dataclass

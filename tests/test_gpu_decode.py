@@ -30,6 +30,8 @@ SHAPES = {
     "tiny_bf16": W.TINY_BF16,
     # real 8B widths, 2 layers, a reduced vocabulary for the host-side LM head
     "llama8b_2l": dataclasses.replace(W.LLAMA8B.with_layers(2), vocab=2048),
+    # the paper's model family: per-head q/k RMSNorm
+    "qwen3_8b_2l": dataclasses.replace(W.QWEN3_8B.with_layers(2), vocab=2048),
 }
 
 
@@ -103,9 +105,13 @@ def test_decode_step_matches_oracle(oracle_lib, name):
     wl = resume_workload(shape, prefix, steps=2, seed=201)
     pre, last = split_last(wl)
     say(f"[decode parity] {name}: prefixes {prefix}")
-    host_w = W.host_weights(shape, seed=41, gain_std=0.1)
     head = W.host_head_weights(shape, seed=42)
-    model = Hn.device_model_from_host(shape, host_w)
+    if shape.hidden <= 512:
+        host_w = W.host_weights(shape, seed=41, gain_std=0.1)
+        model = Hn.device_model_from_host(shape, host_w)
+    else:
+        model = Hn.device_model_random(shape, seed=41, gain_std=0.1)
+        host_w = Hn.host_copy_all(model)
     head_dev = Hn.device_head_from_host(shape, head)
     image = W.host_arena(pre)
     arena = Hn.DeviceArena(pre, host_image=image)

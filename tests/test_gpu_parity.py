@@ -244,6 +244,40 @@ def test_real_width_two_layers(oracle_lib, name, B):
 
 
 # --------------------------------------------------------------------------
+# the Qwen attention variants: per-head q/k RMSNorm, q/k/v bias
+# --------------------------------------------------------------------------
+VARIANT_SHAPES = {
+    "tiny_f32_qknorm_bias": dataclasses.replace(W.TINY_F32, qk_norm=True, qkv_bias=True),
+    "tiny_bf16_qknorm": dataclasses.replace(W.TINY_BF16, qk_norm=True),
+    "tiny_bf16_bias": dataclasses.replace(W.TINY_BF16, qkv_bias=True),
+    "qwen3_8b_2l": W.QWEN3_8B.with_layers(2),
+    "qwen25_1_5b_2l": W.QWEN25_1_5B.with_layers(2),
+}
+
+
+@pytest.mark.parametrize("name", list(VARIANT_SHAPES))
+def test_attention_variants(oracle_lib, name):
+    shape = VARIANT_SHAPES[name]
+    wl = W.small_workload(shape, [1, 17, 300], seed=451, other_live_frac=0.3)
+    say(f"{name} lens={wl.lens.tolist()} qk_norm={shape.qk_norm} qkv_bias={shape.qkv_bias}")
+    if shape.hidden <= 512:
+        host_w = W.host_weights(shape, seed=452, gain_std=0.1)
+        model = Hn.device_model_from_host(shape, host_w)
+    else:
+        model = Hn.device_model_random(shape, seed=452, gain_std=0.1)
+        host_w = Hn.host_copy_all(model)
+    image = W.host_arena(wl)
+    g, arena = gpu_rebuild(wl, model, host_image=image)
+    inv = arena.check_invariants()
+    arena.release()
+    del model
+    torch.cuda.empty_cache()
+    o = oracle_rebuild(oracle_lib, wl, host_w, image)
+    check_parity(wl, g, o, image)
+    assert inv == {"free_changed": 0, "live_changed": 0, "tail_changed": 0, "written_bad": 0}
+
+
+# --------------------------------------------------------------------------
 # the full 8B benchmark workload: sampled layer-0 parity + invariants
 # --------------------------------------------------------------------------
 def test_full_config2_sampled_layer0_and_invariants(oracle_lib):
