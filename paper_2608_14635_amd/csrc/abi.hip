@@ -40,6 +40,24 @@ kv_status ok() {
   return KV_OK;
 }
 
+}  // namespace
+
+// error reporting for the other host files of the library (ipc.hip)
+namespace kvr_err {
+kv_status set(kv_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+kv_status clear() { return ok(); }
+}  // namespace kvr_err
+
+namespace {
+
 int64_t elem_bytes(int32_t dtype) { return dtype == KV_BF16 ? 2 : 4; }
 int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 

@@ -1,5 +1,5 @@
 """Thin ctypes binding of libkvr.so (include/kvr.h, include/kvr_decode.h,
-include/kvr_profile.h).
+include/kvr_ipc.h, include/kvr_profile.h).
 
 Argument marshalling only: every step of the rebuild runs in the library's
 HIP kernels.  Device buffers are passed as integer addresses (for example a
@@ -52,6 +52,11 @@ class kv_weights(C.Structure):
                 ("layers", C.POINTER(kv_layer_weights))]
 
 
+class kv_ipc_handle(C.Structure):
+    _fields_ = [("ipc", C.c_uint8 * 64), ("offset", C.c_uint64), ("bytes", C.c_uint64),
+                ("owner_pid", C.c_int64), ("device", C.c_int32), ("reserved", C.c_int32)]
+
+
 _lib: Optional[C.CDLL] = None
 
 
@@ -97,6 +102,15 @@ def lib() -> C.CDLL:
     L.kv_decode_step.restype = C.c_int
     L.kv_decode_step.argtypes = [C.POINTER(kv_weights), vp, vp, i32p, i32p, C.c_int32, i32p,
                                  C.c_int32, vp, vp, C.c_uint64, vp, vp, vp]
+    hp = C.POINTER(kv_ipc_handle)
+    L.kv_ipc_export.restype = C.c_int
+    L.kv_ipc_export.argtypes = [vp, C.c_uint64, hp]
+    L.kv_ipc_owner_alive.restype = C.c_int
+    L.kv_ipc_owner_alive.argtypes = [hp]
+    L.kv_ipc_open.restype = C.c_int
+    L.kv_ipc_open.argtypes = [hp, C.POINTER(vp)]
+    L.kv_ipc_close.restype = C.c_int
+    L.kv_ipc_close.argtypes = [vp]
     L.kv_profile_enable.restype = C.c_int
     L.kv_profile_enable.argtypes = [vp, C.c_int32]
     L.kv_profile_read.restype = C.c_int
@@ -242,6 +256,42 @@ def kv_decode_step(weights: Weights, final_norm: int, lm_head: int, tokens, posi
                                 C.c_void_p(next_tokens), C.c_void_p(logits or None)))
 
 
+def kv_ipc_export(ptr: int, nbytes: int) -> bytes:
+    """Owner side: the handle of device memory [ptr, ptr+nbytes) as plain bytes."""
+    h = kv_ipc_handle()
+    _check(lib().kv_ipc_export(C.c_void_p(ptr), nbytes, C.byref(h)))
+    return bytes(h)
+
+
+def _handle(blob: bytes) -> kv_ipc_handle:
+    if len(blob) != C.sizeof(kv_ipc_handle):
+        raise ValueError(f"an IPC handle is {C.sizeof(kv_ipc_handle)} bytes, got {len(blob)}")
+    return kv_ipc_handle.from_buffer_copy(blob)
+
+
+def kv_ipc_handle_info(blob: bytes) -> Dict[str, int]:
+    h = _handle(blob)
+    return {"offset": h.offset, "bytes": h.bytes, "owner_pid": h.owner_pid, "device": h.device}
+
+
+def kv_ipc_owner_alive(blob: bytes) -> int:
+    """Status code: KV_OK when the owner process exists, KV_ESTATE when it is gone."""
+    h = _handle(blob)
+    return int(lib().kv_ipc_owner_alive(C.byref(h)))
+
+
+def kv_ipc_open(blob: bytes) -> int:
+    """Importer side: the device address the owner exported."""
+    h = _handle(blob)
+    p = C.c_void_p()
+    _check(lib().kv_ipc_open(C.byref(h), C.byref(p)))
+    return p.value
+
+
+def kv_ipc_close(ptr: int) -> None:
+    _check(lib().kv_ipc_close(C.c_void_p(ptr)))
+
+
 def kv_profile_enable(arena: int, enable: bool = True) -> None:
     _check(lib().kv_profile_enable(C.c_void_p(arena), 1 if enable else 0))
 
@@ -262,4 +312,5 @@ def exported_symbols() -> Iterable[str]:
     return ("kv_arena_bind", "kv_arena_release", "kv_rebuild_workspace_bytes", "kv_rebuild_check",
             "kv_rebuild", "kv_rebuild_stage", "kv_rebuild_execute", "kv_plan_release",
             "kv_plan_info", "kv_last_error", "kv_profile_enable", "kv_profile_read",
-            "kv_profile_reset", "kv_decode_workspace_bytes", "kv_decode_check", "kv_decode_step")
+            "kv_profile_reset", "kv_decode_workspace_bytes", "kv_decode_check", "kv_decode_step",
+            "kv_ipc_export", "kv_ipc_owner_alive", "kv_ipc_open", "kv_ipc_close")

@@ -243,3 +243,47 @@ def test_decode_step_rejects_unknown_arena(L):
     with pytest.raises(kvr.KvError) as e:
         kvr.kv_decode_step(w, 0x1000, 0x1000, toks, pos, tables, 0x1234, 0x10000, 1 << 20, 0x2000)
     assert e.value.status == kvr.KV_ESTATE
+
+
+def _blob(pid: int, device: int = 0) -> bytes:
+    h = kvr.kv_ipc_handle()
+    h.owner_pid, h.device, h.bytes = pid, device, 4096
+    return bytes(h)
+
+
+def _dead_pid() -> int:
+    import subprocess
+    import sys
+    p = subprocess.Popen([sys.executable, "-c", "pass"])
+    p.wait()
+    return p.pid
+
+
+def test_ipc_handle_is_plain_bytes(L):
+    assert C.sizeof(kvr.kv_ipc_handle) == 96
+    info = kvr.kv_ipc_handle_info(_blob(1234, 3))
+    assert info == {"offset": 0, "bytes": 4096, "owner_pid": 1234, "device": 3}
+    with pytest.raises(ValueError):
+        kvr.kv_ipc_handle_info(b"\0" * 95)
+
+
+def test_ipc_owner_liveness(L):
+    assert kvr.kv_ipc_owner_alive(_blob(os.getpid())) == kvr.KV_OK
+    assert kvr.kv_ipc_owner_alive(_blob(os.getppid())) == kvr.KV_OK
+    assert kvr.kv_ipc_owner_alive(_blob(_dead_pid())) == kvr.KV_ESTATE
+    assert kvr.kv_ipc_owner_alive(_blob(0)) == kvr.KV_EINVAL
+
+
+def test_ipc_open_refuses_before_device_access(L):
+    # a dead owner: the state it held is gone, nothing is mapped
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_ipc_open(_blob(_dead_pid()))
+    assert e.value.status == kvr.KV_ESTATE and "gone" in e.value.message
+    # the owner itself may not import its own allocation
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_ipc_open(_blob(os.getpid()))
+    assert e.value.status == kvr.KV_EINVAL
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_ipc_close(0x1000)
+    assert e.value.status == kvr.KV_ESTATE
+    assert L.kv_ipc_export(None, 16, None) == kvr.KV_EINVAL
