@@ -79,6 +79,12 @@ class Oracle:
         self.lib.kvo_time_layers.restype = C.c_int
         self.lib.kvo_time_layers.argtypes = [C.POINTER(_Model), C.c_void_p, C.POINTER(_Layer),
                                              I32P, C.c_int32, C.c_int32]
+        self.lib.kvo_block_digest.restype = C.c_uint64
+        self.lib.kvo_block_digest.argtypes = [C.POINTER(_Model), C.POINTER(_Arena), C.c_int64,
+                                              C.c_int32, C.POINTER(C.c_int)]
+        self.lib.kvo_verify.restype = C.c_int
+        self.lib.kvo_verify.argtypes = [C.POINTER(_Model), C.POINTER(_Arena), I32P, C.c_int32, I32P,
+                                        C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
         self.lib.kvo_round_bf16.restype = C.c_uint16
         self.lib.kvo_round_bf16.argtypes = [C.c_float]
         self.lib.kvo_num_threads.restype = C.c_int
@@ -211,6 +217,48 @@ class Oracle:
         if rc != 0:
             raise ValueError("oracle rejected its arguments")
         return t1 - t0
+
+    def _arena(self, shape, arena: np.ndarray, block_size: int, num_blocks: int, dt: int):
+        need = shape.num_layers * 2 * num_blocks * block_size * shape.num_kv_heads * shape.head_dim
+        assert arena.itemsize == np.dtype(_NP[dt]).itemsize
+        assert arena.flags.c_contiguous and arena.size >= need, "arena smaller than its geometry"
+        return _Arena(arena.ctypes.data, block_size, num_blocks)
+
+    def block_digest(self, shape, arena: np.ndarray, block_size: int, num_blocks: int, block: int,
+                     nslots: int, dtype: Optional[int] = None) -> int:
+        """Commit digest of slots [0, nslots) of one block (kvo.h defines it)."""
+        dt = shape.dtype if dtype is None else dtype
+        m = self._model(shape, dt)
+        ar = self._arena(shape, arena, block_size, num_blocks, dt)
+        ok = C.c_int()
+        v = self.lib.kvo_block_digest(C.byref(m), C.byref(ar), block, nslots, C.byref(ok))
+        if ok.value != 0:
+            raise ValueError("oracle rejected its arguments")
+        return int(v)
+
+    def verify(self, shape, arena: np.ndarray, block_size: int, num_blocks: int, lens, tables,
+               committed=None, dtype: Optional[int] = None):
+        """(digests [entries] uint64, intact [R] int32): every used block's
+        digest, request by request, and the count of leading blocks per request
+        whose digest equals `committed` (all zeros when committed is None)."""
+        dt = shape.dtype if dtype is None else dtype
+        m = self._model(shape, dt)
+        ar = self._arena(shape, arena, block_size, num_blocks, dt)
+        lens, tables = self._i32(lens), self._i32(tables)
+        max_blocks = tables.shape[1] if tables.ndim == 2 else 0
+        n = int(sum((int(x) + block_size - 1) // block_size for x in lens))
+        dg = np.zeros(max(n, 1), np.uint64)
+        com = (np.zeros(max(n, 1), np.uint64) if committed is None
+               else np.ascontiguousarray(committed, dtype=np.uint64))
+        assert com.size >= n
+        intact = np.zeros(max(len(lens), 1), np.int32)
+        I32P = C.POINTER(C.c_int32)
+        rc = self.lib.kvo_verify(C.byref(m), C.byref(ar), lens.ctypes.data_as(I32P), len(lens),
+                                 tables.ctypes.data_as(I32P), max_blocks, com.ctypes.data,
+                                 dg.ctypes.data, intact.ctypes.data)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        return dg[:n], intact[:len(lens)]
 
     def round_bf16(self, x: float) -> int:
         return int(self.lib.kvo_round_bf16(float(x)))

@@ -485,3 +485,61 @@ int kvo_time_layers(const kvo_model* m, const void* embed, const kvo_layer* laye
   free(table);
   return rc;
 }
+
+/* ------------------------------------------------------------------ */
+/* commit digests of arena blocks (flush-free recovery)                */
+/* ------------------------------------------------------------------ */
+static int64_t elem_bytes(int dtype) { return dtype == KVO_F64 ? 8 : (dtype == KVO_F32 ? 4 : 2); }
+
+uint64_t kvo_block_digest(const kvo_model* m, const kvo_arena* a, int64_t block, int32_t nslots,
+                          int* ok) {
+  const int64_t row = (int64_t)m->num_kv_heads * m->head_dim * elem_bytes(m->dtype);
+  const uint8_t* base = (const uint8_t*)a->base;
+  uint64_t sum = 0;
+  uint32_t i = 0; /* word index, counted modulo 2^32 */
+  int l, kv;
+  int32_t s;
+  int64_t w;
+  *ok = -1;
+  if (row % 4 != 0 || block < 0 || block >= a->num_blocks || nslots < 0 || nslots > a->block_size)
+    return 0;
+  for (l = 0; l < m->num_layers; ++l)
+    for (kv = 0; kv < 2; ++kv)
+      for (s = 0; s < nslots; ++s) {
+        const int64_t slot = block * a->block_size + s;
+        const uint8_t* p = base + arena_off(m, a, l, kv, slot) * elem_bytes(m->dtype);
+        for (w = 0; w < row / 4; ++w, ++i) {
+          const uint32_t u = (uint32_t)p[4 * w] | (uint32_t)p[4 * w + 1] << 8 |
+                             (uint32_t)p[4 * w + 2] << 16 | (uint32_t)p[4 * w + 3] << 24;
+          const uint32_t x = u ^ (uint32_t)(i * 0x9E3779B9u);
+          sum += (uint64_t)x * (uint64_t)x;
+        }
+      }
+  *ok = 0;
+  return sum;
+}
+
+int kvo_verify(const kvo_model* m, const kvo_arena* a, const int32_t* lens, int32_t R,
+               const int32_t* tables, int32_t max_blocks, const uint64_t* committed,
+               uint64_t* digests, int32_t* intact) {
+  const int32_t B = a->block_size;
+  int64_t e = 0;
+  int32_t r, j;
+  if (!m || !a || !a->base || B <= 0 || R < 0 || !committed || !intact) return -1;
+  for (r = 0; r < R; ++r) {
+    const int32_t nb = (lens[r] + B - 1) / B;
+    int leading = 1;
+    if (lens[r] < 0 || nb > max_blocks) return -1;
+    intact[r] = 0;
+    for (j = 0; j < nb; ++j, ++e) {
+      const int32_t n = lens[r] - j * B < B ? lens[r] - j * B : B;
+      int ok;
+      const uint64_t dg = kvo_block_digest(m, a, tables[(int64_t)r * max_blocks + j], n, &ok);
+      if (ok != 0) return -1;
+      if (digests) digests[e] = dg;
+      if (leading && dg == committed[e]) intact[r] = j + 1;
+      else leading = 0;
+    }
+  }
+  return 0;
+}

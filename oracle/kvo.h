@@ -106,6 +106,30 @@ int kvo_layer0_kv(const kvo_model* m, const void* embed, const kvo_layer* layer0
 int kvo_time_layers(const kvo_model* m, const void* embed, const kvo_layer* layers,
                     const int32_t* tokens, int32_t n, int32_t num_layers);
 
+/* Commit digest of one block (flush-free recovery; the paper flushes the
+ * whole pool because it cannot tell which KV contents survived intact, and
+ * leaves fine-grained consistency tracking to future work: Sec. 4.2 flush
+ * paragraph, Sec. 8 future work).  The digest covers slots 0 .. nslots-1 of
+ * `block` in every layer and both planes.  Read those bytes as 32-bit
+ * little-endian words u_0 .. u_{N-1} in the order (layer, K then V, slot, byte
+ * within the slot row), N = num_layers * 2 * nslots * row_bytes / 4; then
+ *     digest = sum over i of (u_i XOR (i * 0x9E3779B9 mod 2^32))^2  mod 2^64
+ * (the square taken as a 64-bit product of two 32-bit values).  nslots = 0
+ * gives 0.  Returns -1 in *ok on invalid arguments (row bytes not a multiple
+ * of 4, block or nslots out of range), else 0. */
+uint64_t kvo_block_digest(const kvo_model* m, const kvo_arena* a, int64_t block, int32_t nslots,
+                          int* ok);
+
+/* Verify the committed digests of a request set: request r occupies blocks
+ * tables[r][0 .. ceil(lens[r]/B)-1]; block j of it covers min(B, lens[r]-j*B)
+ * slots.  Entries are numbered request by request, block by block.  Writes
+ * every entry's digest to digests (may be NULL) and, per request, the number
+ * of leading blocks whose digest equals committed[entry] to intact.
+ * Returns 0, or -1 on invalid arguments. */
+int kvo_verify(const kvo_model* m, const kvo_arena* a, const int32_t* lens, int32_t R,
+               const int32_t* tables, int32_t max_blocks, const uint64_t* committed,
+               uint64_t* digests, int32_t* intact);
+
 /* fp32 -> bf16 bits exactly as the oracle rounds (exported for its pins). */
 uint16_t kvo_round_bf16(float x);
 

@@ -17,6 +17,9 @@ What pins what:
     GQA == MHA with duplicated KV heads; causality; batch independence;
     idempotence over garbage; exact placement and untouched bits
   * library routine: fp32 -> bf16 rounding against torch's conversion
+  * block commit digests: closed forms on arenas built to cancel the word
+    keys (N c^2, one changed word), bit flips always detected, bytes outside
+    the covered slots ignored, leading-intact counts with planted corruption
 """
 from __future__ import annotations
 
@@ -595,6 +598,137 @@ def pin_resume_from_rebuild_equals_decode_built(o):
         t_de, z_de, a_de = _resume(o, shape, w, head, wl, "decode", 5)
         assert np.array_equal(t_re, t_de) and np.array_equal(z_re, z_de)
         assert np.array_equal(a_re, a_de)
+
+
+# --------------------------------------------------------------------------
+# block commit digests
+# --------------------------------------------------------------------------
+DIGEST_GEOMS = (dataclasses.replace(W.TINY_F32, num_layers=3, num_q_heads=2, num_kv_heads=2, head_dim=8),
+                dataclasses.replace(W.TINY_BF16, num_layers=2, num_q_heads=6, num_kv_heads=3, head_dim=8))
+GOLDEN = 0x9E3779B9
+M64 = (1 << 64) - 1
+
+
+def _digest_arena(shape, B=4, NB=5, seed=0):
+    """Random raw arena bits plus its 32-bit word view [L, 2, NB, B, words per row]."""
+    rng = np.random.default_rng(seed)
+    el = np.uint16 if shape.dtype == BF16 else np.uint32
+    n = shape.num_layers * 2 * NB * B * shape.num_kv_heads * shape.head_dim
+    a = rng.integers(0, np.iinfo(el).max, size=n, dtype=el, endpoint=True)
+    wr = shape.num_kv_heads * shape.head_dim * a.itemsize // 4
+    return a, a.view(np.uint32).reshape(shape.num_layers, 2, NB, B, wr)
+
+
+def _keys(n):
+    return ((np.arange(n, dtype=np.uint64) * np.uint64(GOLDEN)) & np.uint64(0xFFFFFFFF)).astype(np.uint32)
+
+
+def pin_digest_keyed_closed_form(o):
+    """Covered words set to key_i XOR c (keys in the order layer, K|V, slot,
+    word) make every squared term c^2: digest = N c^2 mod 2^64, whatever the
+    bytes outside the covered slots hold; c = 0 gives 0; nslots = 0 gives 0."""
+    for shape in DIGEST_GEOMS:
+        for blk, ns, c in ((0, 4, 0), (2, 3, 1), (4, 1, 0xFFFFFFFF), (3, 2, 0x12345678)):
+            a, words = _digest_arena(shape, seed=blk)
+            L, _, NB, B, wr = words.shape
+            N = L * 2 * ns * wr
+            words[:, :, blk, :ns, :] = (_keys(N) ^ np.uint32(c)).reshape(L, 2, ns, wr)
+            got = o.block_digest(shape, a, B, NB, blk, ns)
+            assert got == (N * c * c) & M64, (shape.dtype, blk, ns, c, got)
+        assert o.block_digest(shape, a, B, NB, 1, 0) == 0
+
+
+def pin_digest_one_changed_word(o):
+    """From the keyed arena, word j set to key_j XOR c' gives
+    (N-1) c^2 + c'^2 mod 2^64, for words at plane, slot and row boundaries."""
+    for shape in DIGEST_GEOMS:
+        a, words = _digest_arena(shape, seed=7)
+        L, _, NB, B, wr = words.shape
+        blk, ns, c = 1, 3, 0xDEADBEEF
+        N = L * 2 * ns * wr
+        keys = _keys(N)
+        view = words[:, :, blk, :ns, :]
+        view[...] = (keys ^ np.uint32(c)).reshape(L, 2, ns, wr)
+        for j in (0, wr - 1, wr, ns * wr - 1, ns * wr, N // 2 + 1, N - wr, N - 1):
+            l, rem = divmod(j, 2 * ns * wr)
+            kv, rem = divmod(rem, ns * wr)
+            s, w = divmod(rem, wr)
+            for c2 in (0, 5, 0xFFFFFFFF):
+                saved = view[l, kv, s, w]
+                view[l, kv, s, w] = keys[j] ^ np.uint32(c2)
+                got = o.block_digest(shape, a, B, NB, blk, ns)
+                view[l, kv, s, w] = saved
+                assert got == ((N - 1) * c * c + c2 * c2) & M64, (shape.dtype, j, c2)
+
+
+def pin_digest_detects_every_bit_flip(o):
+    """Changing one 32-bit word x to x' changes (x^k)^2 by a nonzero amount
+    below 2^64 in magnitude, so any change of one covered word is detected;
+    check every bit of a few words of each plane."""
+    for shape in DIGEST_GEOMS:
+        a, words = _digest_arena(shape, seed=11)
+        L, _, NB, B, wr = words.shape
+        blk, ns = 2, B
+        ref = o.block_digest(shape, a, B, NB, blk, ns)
+        for l in range(L):
+            for kv in range(2):
+                for (s, w) in ((0, 0), (B - 1, wr - 1)):
+                    for bit in range(32):
+                        words[l, kv, blk, s, w] ^= np.uint32(1 << bit)
+                        assert o.block_digest(shape, a, B, NB, blk, ns) != ref, (l, kv, s, w, bit)
+                        words[l, kv, blk, s, w] ^= np.uint32(1 << bit)
+        assert o.block_digest(shape, a, B, NB, blk, ns) == ref
+
+
+def pin_digest_covers_exactly_its_slots(o):
+    """Bytes of other blocks and of slots >= nslots do not enter the digest;
+    the same contents moved to another block give the same digest."""
+    for shape in DIGEST_GEOMS:
+        a, words = _digest_arena(shape, seed=13)
+        L, _, NB, B, wr = words.shape
+        blk, ns = 3, 2
+        ref = o.block_digest(shape, a, B, NB, blk, ns)
+        rng = np.random.default_rng(5)
+        for other in range(NB):
+            if other != blk:
+                words[:, :, other] = rng.integers(0, 2**32, size=words[:, :, other].shape, dtype=np.uint64).astype(np.uint32)
+        words[:, :, blk, ns:] = 0
+        assert o.block_digest(shape, a, B, NB, blk, ns) == ref
+        words[:, :, 0, :ns] = words[:, :, blk, :ns]
+        assert o.block_digest(shape, a, B, NB, 0, ns) == ref
+        assert o.block_digest(shape, a, B, NB, blk, ns + 1) != ref
+
+
+def pin_verify_leading_intact_counts(o):
+    """Committed digests of a rebuilt arena, then corruption planted in chosen
+    blocks: each request's leading-intact count is the index of its first
+    corrupted block; tail slots past a request's length and blocks of other
+    requests do not count against it."""
+    shape = W.TINY_F32
+    w = W.host_weights(shape, seed=41)
+    wl = W.small_workload(shape, [5, 16, 33, 0, 47], block_size=8, seed=141, other_live_frac=0.2)
+    image = W.host_arena(wl)
+    o.rebuild(shape, w, wl.tokens, wl.lens, wl.block_tables, image, wl.block_size, wl.num_blocks)
+    committed, intact = o.verify(shape, image, wl.block_size, wl.num_blocks, wl.lens, wl.block_tables)
+    nb = (wl.lens + wl.block_size - 1) // wl.block_size
+    assert committed.size == nb.sum() and np.all(intact == 0) or nb.sum() == 0
+    _, intact = o.verify(shape, image, wl.block_size, wl.num_blocks, wl.lens, wl.block_tables, committed)
+    assert np.array_equal(intact, nb)
+    B = wl.block_size
+    row = shape.num_kv_heads * shape.head_dim
+    arena6 = image.view(np.float32).reshape(shape.num_layers, 2, wl.num_blocks, B, row)
+    # tail slots of request 2 (33 tokens: block 4 holds slot 0 only) and a free block
+    arena6[1, 0, wl.block_tables[2, 4], 1:] = np.float32(7.0)
+    for b in wl.other_live[:2]:
+        arena6[0, 1, b] += np.float32(1.0)
+    _, intact = o.verify(shape, image, B, wl.num_blocks, wl.lens, wl.block_tables, committed)
+    assert np.array_equal(intact, nb)
+    # request 1: block 1 (V plane, last layer); request 4: block 2 and block 5
+    arena6[shape.num_layers - 1, 1, wl.block_tables[1, 1], B - 1, row - 1] *= np.float32(-1.0)
+    arena6[0, 0, wl.block_tables[4, 2], 0, 0] = np.float32(0.5)
+    arena6[0, 0, wl.block_tables[4, 5], 0, 0] = np.float32(0.25)
+    _, intact = o.verify(shape, image, B, wl.num_blocks, wl.lens, wl.block_tables, committed)
+    assert intact.tolist() == [nb[0], 1, nb[2], 0, 2], intact.tolist()
 
 
 PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -52,6 +52,19 @@ MUTANTS = [
      "to_work(dot_row(W, dt, i, K, A + r * K), dt)", 0),
     ("v_bias_from_k", "project_bias(lw->wv, lw->bv, dt, nkv * d, H, a, cnt, v);",
      "project_bias(lw->wv, lw->bk, dt, nkv * d, H, a, cnt, v);", 0),
+    ("digest_key_multiplier", "u ^ (uint32_t)(i * 0x9E3779B9u)", "u ^ (uint32_t)(i * 0x9E3779B1u)", 0),
+    ("digest_unkeyed", "u ^ (uint32_t)(i * 0x9E3779B9u)", "u", 0),
+    ("digest_key_restarts_per_plane", "for (s = 0; s < nslots; ++s) {", "for (s = 0, i = 0; s < nslots; ++s) {", 0),
+    ("digest_big_endian_words", "(uint32_t)p[4 * w] | (uint32_t)p[4 * w + 1] << 8 |",
+     "(uint32_t)p[4 * w + 3] | (uint32_t)p[4 * w + 2] << 8 |", 0),
+    ("digest_one_slot_too_many", "for (s = 0; s < nslots; ++s) {", "for (s = 0; s <= nslots && s < a->block_size; ++s) {", 0),
+    ("digest_k_plane_only", "for (kv = 0; kv < 2; ++kv)\n      for (s = 0; s < nslots",
+     "for (kv = 0; kv < 1; ++kv)\n      for (s = 0; s < nslots", 0),
+    ("digest_linear_not_square", "sum += (uint64_t)x * (uint64_t)x;", "sum += (uint64_t)x;", 0),
+    ("verify_counts_all_matches", "if (leading && dg == committed[e]) intact[r] = j + 1;",
+     "if (dg == committed[e]) intact[r] += 1;", 0),
+    ("verify_tail_block_full", "const int32_t n = lens[r] - j * B < B ? lens[r] - j * B : B;",
+     "const int32_t n = B;", 0),
 ]
 
 
