@@ -112,6 +112,69 @@ def resume_decode(wl, model, arena, Hn, kvr, W, steps, stream, log):
     return out
 
 
+def flush_free(wl, model, arena, ws_rebuild, Hn, kvr, reps, stream, log):
+    """Flush-free recovery over the rebuilt arena: commit digests of every
+    block the requests occupy, then time the verification scan (HBM-bound:
+    every covered byte read once, HIP events on the library's stream), and
+    one recovery of a single damaged request (verify + rebuild of that request
+    only) against the full flush-and-refill rebuild."""
+    import numpy as np
+    import torch
+    s, B = wl.shape, wl.block_size
+    E = kvr.num_entries(wl.lens, B)
+    R = wl.num_requests
+    nbytes = kvr.kv_verify_workspace_bytes(R, E)
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+    committed = torch.empty(max(E, 1), dtype=torch.int64, device="cuda")
+    intact = torch.empty(max(R, 1), dtype=torch.int32, device="cuda")
+    kvr.kv_block_digests(arena.handle, wl.lens, wl.block_tables, ws.data_ptr(), nbytes,
+                         committed.data_ptr(), stream)
+
+    def verify():
+        kvr.kv_verify(arena.handle, wl.lens, wl.block_tables, committed.data_ptr(), ws.data_ptr(),
+                      nbytes, intact.data_ptr(), 0, stream)
+    verify()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        verify()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nb = (wl.lens + B - 1) // B
+    all_intact = bool(np.array_equal(intact[:R].cpu().numpy(), nb))
+    covered = int(wl.lens.astype(np.int64).sum()) * s.num_layers * 2 * s.num_kv_heads * s.head_dim * s.elem_bytes
+    moved = covered + 8 * E + E + 4 * (R + 1) + 8 * E + 4 * R
+    # one damaged request (the median-length one): verify, then rebuild it alone
+    r = int(np.argsort(wl.lens)[R // 2])
+    blk = int(wl.block_tables[r, int(nb[r]) // 2])
+    arena.bits[s.num_layers - 1, 1, blk, 0, 0, 0] ^= 1
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    verify()
+    got = intact[:R].cpu().numpy()
+    bad = np.nonzero(got < nb)[0]
+    offs = wl.request_offsets()
+    toks = np.concatenate([wl.tokens[offs[i]:offs[i] + wl.lens[i]] for i in bad]) if bad.size else \
+        np.zeros(0, np.int32)
+    kvr.kv_rebuild(model.weights, toks, wl.lens[bad], wl.block_tables[bad], arena.handle,
+                   ws_rebuild[0].data_ptr(), ws_rebuild[1], stream)
+    torch.cuda.synchronize()
+    rec_ms = (time.perf_counter() - t0) * 1e3
+    verify()
+    healed = bool(np.array_equal(intact[:R].cpu().numpy(), nb))
+    out = {"entries": E, "verify_ms": ms, "covered_bytes": covered, "bytes_per_launch": moved,
+           "achieved_GBps": moved / (ms / 1e3) / 1e9, "hbm_frac": moved / (ms / 1e3) / 1e9 / PEAK_HBM_GBS,
+           "all_intact_after_rebuild": all_intact,
+           "one_damaged_request": {"request": r, "tokens": int(wl.lens[r]),
+                                   "detected": bad.tolist(), "recovery_ms": rec_ms,
+                                   "intact_after": healed}}
+    log(f"[bench] verify scan: {ms:.3f} ms over {E} blocks, {out['achieved_GBps']:.0f} GB/s "
+        f"({100 * out['hbm_frac']:.1f}% of HBM); one damaged request recovered in {rec_ms:.1f} ms")
+    return out
+
+
 def algorithmic_work(wl):
     """Flops and HBM bytes the method must spend (last layer: K/V projections only)."""
     s = wl.shape
@@ -191,6 +254,8 @@ def main():
     ap.add_argument("--no-check", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=4,
                     help="resumed-decode steps timed after the rebuild (0 = none)")
+    ap.add_argument("--verify-reps", type=int, default=20,
+                    help="timed block-digest verification scans after the rebuild (0 = skip)")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="only copy this many bytes device-to-device (counter calibration)")
     args = ap.parse_args()
@@ -301,6 +366,10 @@ def main():
     if args.decode_steps > 0 and wl.num_requests > 0:
         dec = resume_decode(wl, model, arena, Hn, kvr, W, args.decode_steps, stream, log)
 
+    ff = None
+    if args.verify_reps > 0 and wl.num_requests > 0:
+        ff = flush_free(wl, model, arena, (ws, nbytes), Hn, kvr, args.verify_reps, stream, log)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
@@ -337,6 +406,7 @@ def main():
                            for k, v in prof.items()},
         "arena_check": check,
         "resume_decode": dec,
+        "flush_free": ff,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

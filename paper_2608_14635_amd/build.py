@@ -20,7 +20,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libkvr.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["abi.hip", "misc.hip", "gemm_bf16.hip", "gemm_f32.hip", "attention.hip", "decode.hip", "ipc.hip"]
+SOURCES = ["abi.hip", "misc.hip", "gemm_bf16.hip", "gemm_f32.hip", "attention.hip", "decode.hip", "ipc.hip", "verify.hip"]
 # Device code is built without packed-fp32 instructions (the host pass warns
 # that it does not know the feature; that is expected).
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC,

@@ -16,6 +16,7 @@
 
 #include "kvr.h"
 #include "kvr_decode.h"
+#include "kvr_verify.h"
 #include "kvr_profile.h"
 #include "launch.h"
 
@@ -1113,6 +1114,154 @@ kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void
   const hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(KV_EDEVICE, "kernel launch failed: %s", hipGetErrorString(err));
   return ok();
+}
+
+// ---------------------------------------------------------------------------
+// Block commit digests and verification (kvr_verify.h)
+// ---------------------------------------------------------------------------
+namespace {
+
+// Workspace: the staged entry list (block, covered slots) and request offsets,
+// then the per-entry match flags and a digest buffer for calls that do not
+// want the digests back.
+struct VerifyLayout {
+  size_t entries = 0, offsets = 0, meta_end = 0, match = 0, digests = 0, total = 0;
+};
+
+VerifyLayout make_verify_layout(int32_t R, int64_t E) {
+  VerifyLayout L;
+  size_t off = 0;
+  auto seg = [&](size_t bytes) {
+    const size_t at = off;
+    off = (size_t)round_up((int64_t)(off + bytes), 256);
+    return at;
+  };
+  L.entries = seg(8 * (size_t)E);
+  L.offsets = seg(4 * ((size_t)R + 1));
+  L.meta_end = off;
+  L.match = seg((size_t)E);
+  L.digests = seg(8 * (size_t)E);
+  L.total = off;
+  return L;
+}
+
+kv_status verify_impl(kv_arena* arena, const int32_t* lens, int32_t R, const int32_t* tables,
+                      int32_t max_blocks, const uint64_t* committed, void* workspace,
+                      uint64_t ws_bytes, void* stream, uint64_t* digests, int32_t* intact) {
+  if (!live_arena(arena)) return fail(KV_ESTATE, "unknown or released arena handle");
+  if (R < 0) return fail(KV_EINVAL, "num_requests < 0");
+  if (R > 0 && (!lens || !tables)) return fail(KV_EINVAL, "null lens or block tables");
+  const kv_model_desc& d = arena->desc;
+  const int64_t row = (int64_t)d.num_kv_heads * d.head_dim * elem_bytes(d.dtype);
+  if (row % 16 != 0) return fail(KV_EINVAL, "slot row of %lld bytes is not a multiple of 16", (long long)row);
+  const int32_t B = arena->block_size;
+  int64_t E = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    if (lens[r] < 0) return fail(KV_EINVAL, "request %d has length %d", r, lens[r]);
+    const int64_t nb = ((int64_t)lens[r] + B - 1) / B;
+    if (nb > max_blocks)
+      return fail(KV_ECAPACITY, "request %d needs %lld blocks > %d table entries", r, (long long)nb, max_blocks);
+    for (int64_t j = 0; j < nb; ++j) {
+      const int32_t b = tables[(int64_t)r * max_blocks + j];
+      if (b < 0 || b >= arena->num_blocks)
+        return fail(KV_ERANGE, "request %d block %lld is %d, outside [0, %lld)", r, (long long)j, b,
+                    (long long)arena->num_blocks);
+    }
+    E += nb;
+  }
+  if (E > 0x7fffffffLL) return fail(KV_EINVAL, "more than 2^31-1 blocks");
+  if (E > 0 && !committed && !digests) return fail(KV_EINVAL, "null digest output");
+  if (committed && R > 0 && !intact) return fail(KV_EINVAL, "null intact output");
+  if (R == 0) return ok();
+  if (!workspace) return fail(KV_EINVAL, "null workspace");
+  const VerifyLayout L = make_verify_layout(R, E);
+  if (L.total > ws_bytes)
+    return fail(KV_ENOMEM, "workspace of %llu bytes < %llu needed", (unsigned long long)ws_bytes,
+                (unsigned long long)L.total);
+  DeviceGuard dg(arena->device);
+  if (dg.err != hipSuccess) return fail(KV_EDEVICE, "cannot select device %d", arena->device);
+  {
+    const hipError_t pre = hipGetLastError();
+    if (pre != hipSuccess) return fail(KV_EDEVICE, "pending device error: %s", hipGetErrorString(pre));
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  char* ws = reinterpret_cast<char*>(workspace);
+
+  if (arena->staged_pending) {
+    (void)hipEventSynchronize(arena->staged);
+    arena->staged_pending = false;
+  }
+  if (arena->pinned_bytes < L.meta_end) {
+    if (arena->pinned) (void)hipHostFree(arena->pinned);
+    arena->pinned = nullptr;
+    arena->pinned_bytes = 0;
+    if (hipHostMalloc(&arena->pinned, L.meta_end, hipHostMallocDefault) != hipSuccess) {
+      arena->pinned = nullptr;
+      return fail(KV_ENOMEM, "pinned staging allocation of %zu bytes failed", (size_t)L.meta_end);
+    }
+    arena->pinned_bytes = L.meta_end;
+  }
+  char* hb = reinterpret_cast<char*>(arena->pinned);
+  int2* hent = reinterpret_cast<int2*>(hb + L.entries);
+  int32_t* hoff = reinterpret_cast<int32_t*>(hb + L.offsets);
+  int64_t e = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    hoff[r] = (int32_t)e;
+    const int32_t nb = (lens[r] + B - 1) / B;
+    for (int32_t j = 0; j < nb; ++j, ++e)
+      hent[e] = make_int2(tables[(int64_t)r * max_blocks + j], std::min(B, lens[r] - j * B));
+  }
+  hoff[R] = (int32_t)e;
+  {
+    hipError_t err = hipMemcpyAsync(ws, hb, L.meta_end, hipMemcpyHostToDevice, s);
+    if (err == hipSuccess) err = hipEventRecord(arena->staged, s);
+    if (err != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(KV_EDEVICE, "metadata upload failed: %s", hipGetErrorString(err));
+    }
+    arena->staged_pending = true;
+  }
+  DigestParams p;
+  p.arena = reinterpret_cast<const char*>(arena->base);
+  p.block_bytes = (int64_t)B * row;
+  p.plane_bytes = arena->num_blocks * p.block_bytes;
+  p.row_bytes = (int32_t)row;
+  p.planes = 2 * d.num_layers;
+  p.entries = reinterpret_cast<const int2*>(ws + L.entries);
+  p.num_entries = E;
+  p.committed = committed;
+  p.digests = digests ? digests : reinterpret_cast<uint64_t*>(ws + L.digests);
+  p.match = reinterpret_cast<uint8_t*>(ws + L.match);
+  launch_block_digest(p, s);
+  if (committed)
+    launch_leading_intact(reinterpret_cast<const int32_t*>(ws + L.offsets), R, p.match, intact, s);
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(KV_EDEVICE, "kernel launch failed: %s", hipGetErrorString(err));
+  return ok();
+}
+
+}  // namespace
+
+uint64_t kv_verify_workspace_bytes(int32_t num_requests, int64_t num_entries) {
+  if (num_requests < 0 || num_entries < 0) return 0;
+  return make_verify_layout(num_requests, num_entries).total;
+}
+
+kv_status kv_block_digests(kv_arena_t arena, const int32_t* lens, int32_t num_requests,
+                           const int32_t* block_tables, int32_t max_blocks_per_req,
+                           void* workspace, uint64_t workspace_bytes, void* stream,
+                           uint64_t* digests) {
+  return verify_impl(arena, lens, num_requests, block_tables, max_blocks_per_req, nullptr, workspace,
+                     workspace_bytes, stream, digests, nullptr);
+}
+
+kv_status kv_verify(kv_arena_t arena, const int32_t* lens, int32_t num_requests,
+                    const int32_t* block_tables, int32_t max_blocks_per_req,
+                    const uint64_t* committed, void* workspace, uint64_t workspace_bytes,
+                    void* stream, uint64_t* digests, int32_t* intact) {
+  if (!committed) return fail(KV_EINVAL, "null committed digests");
+  return verify_impl(arena, lens, num_requests, block_tables, max_blocks_per_req, committed,
+                     workspace, workspace_bytes, stream, digests, intact);
 }
 
 // ---------------------------------------------------------------------------

@@ -137,4 +137,25 @@ constexpr int ARGMAX_CHUNKS = 256;  // vocab chunks of the first argmax pass
 void launch_argmax(const float* logits_t, int64_t ld, int vocab, int num_requests,
                    float2* partial, int32_t* next_tokens, float* logits_out, hipStream_t s);
 
+// Block commit digests (flush-free recovery): one workgroup per entry reads
+// the entry's covered slots in every plane and reduces the keyed sum of squares.
+constexpr uint32_t DIGEST_KEY = 0x9E3779B9u;  // word-index multiplier of the key
+struct DigestParams {
+  const char* arena;        // arena base
+  int64_t plane_bytes;      // bytes of one (layer, K|V) plane: num_blocks * block_size * row
+  int64_t block_bytes;      // block_size * row
+  int32_t row_bytes;        // one slot: nkv * d * element bytes (a multiple of 16)
+  int32_t planes;           // 2 * num_layers
+  const int2* entries;      // [n] (block id, covered slots)
+  int64_t num_entries;
+  const uint64_t* committed;  // [n] or null
+  uint64_t* digests;        // [n] or null
+  uint8_t* match;           // [n] digest == committed (written when committed is set)
+};
+void launch_block_digest(const DigestParams& p, hipStream_t s);
+// intact[r] = index of request r's first entry (offsets[r] .. offsets[r+1]-1)
+// whose match flag is 0, or its entry count when all match
+void launch_leading_intact(const int32_t* offsets, int32_t num_requests, const uint8_t* match,
+                           int32_t* intact, hipStream_t s);
+
 }  // namespace kvr

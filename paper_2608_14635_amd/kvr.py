@@ -1,5 +1,5 @@
 """Thin ctypes binding of libkvr.so (include/kvr.h, include/kvr_decode.h,
-include/kvr_ipc.h, include/kvr_profile.h).
+include/kvr_ipc.h, include/kvr_verify.h, include/kvr_profile.h).
 
 Argument marshalling only: every step of the rebuild runs in the library's
 HIP kernels.  Device buffers are passed as integer addresses (for example a
@@ -102,6 +102,12 @@ def lib() -> C.CDLL:
     L.kv_decode_step.restype = C.c_int
     L.kv_decode_step.argtypes = [C.POINTER(kv_weights), vp, vp, i32p, i32p, C.c_int32, i32p,
                                  C.c_int32, vp, vp, C.c_uint64, vp, vp, vp]
+    L.kv_verify_workspace_bytes.restype = C.c_uint64
+    L.kv_verify_workspace_bytes.argtypes = [C.c_int32, C.c_int64]
+    L.kv_block_digests.restype = C.c_int
+    L.kv_block_digests.argtypes = [vp, i32p, C.c_int32, i32p, C.c_int32, vp, C.c_uint64, vp, vp]
+    L.kv_verify.restype = C.c_int
+    L.kv_verify.argtypes = [vp, i32p, C.c_int32, i32p, C.c_int32, vp, vp, C.c_uint64, vp, vp, vp]
     hp = C.POINTER(kv_ipc_handle)
     L.kv_ipc_export.restype = C.c_int
     L.kv_ipc_export.argtypes = [vp, C.c_uint64, hp]
@@ -256,6 +262,37 @@ def kv_decode_step(weights: Weights, final_norm: int, lm_head: int, tokens, posi
                                 C.c_void_p(next_tokens), C.c_void_p(logits or None)))
 
 
+def num_entries(lens, block_size: int) -> int:
+    """Blocks a request set occupies: sum of ceil(len / block_size)."""
+    ln = _i32(lens).astype(np.int64)
+    return int(((ln + block_size - 1) // block_size).sum())
+
+
+def kv_verify_workspace_bytes(num_requests: int, entries: int) -> int:
+    return int(lib().kv_verify_workspace_bytes(num_requests, entries))
+
+
+def kv_block_digests(arena: int, lens, tables, workspace: int, workspace_bytes: int, digests: int,
+                     stream: int = 0) -> None:
+    """Commit digests (device uint64 [entries]) of every block the requests occupy."""
+    ln = _i32(lens)
+    tab, mb = _tables2d(tables, len(ln))
+    _check(lib().kv_block_digests(C.c_void_p(arena), _ptr(ln), len(ln), _ptr(tab), mb,
+                                  C.c_void_p(workspace), workspace_bytes, C.c_void_p(stream),
+                                  C.c_void_p(digests)))
+
+
+def kv_verify(arena: int, lens, tables, committed: int, workspace: int, workspace_bytes: int,
+              intact: int, digests: int = 0, stream: int = 0) -> None:
+    """Per request, the count of leading blocks matching their committed digests
+    (device int32 [R] at `intact`); current digests optionally at `digests`."""
+    ln = _i32(lens)
+    tab, mb = _tables2d(tables, len(ln))
+    _check(lib().kv_verify(C.c_void_p(arena), _ptr(ln), len(ln), _ptr(tab), mb,
+                           C.c_void_p(committed), C.c_void_p(workspace), workspace_bytes,
+                           C.c_void_p(stream), C.c_void_p(digests or None), C.c_void_p(intact)))
+
+
 def kv_ipc_export(ptr: int, nbytes: int) -> bytes:
     """Owner side: the handle of device memory [ptr, ptr+nbytes) as plain bytes."""
     h = kv_ipc_handle()
@@ -313,4 +350,5 @@ def exported_symbols() -> Iterable[str]:
             "kv_rebuild", "kv_rebuild_stage", "kv_rebuild_execute", "kv_plan_release",
             "kv_plan_info", "kv_last_error", "kv_profile_enable", "kv_profile_read",
             "kv_profile_reset", "kv_decode_workspace_bytes", "kv_decode_check", "kv_decode_step",
-            "kv_ipc_export", "kv_ipc_owner_alive", "kv_ipc_open", "kv_ipc_close")
+            "kv_ipc_export", "kv_ipc_owner_alive", "kv_ipc_open", "kv_ipc_close",
+            "kv_verify_workspace_bytes", "kv_block_digests", "kv_verify")

@@ -287,3 +287,24 @@ def test_ipc_open_refuses_before_device_access(L):
         kvr.kv_ipc_close(0x1000)
     assert e.value.status == kvr.KV_ESTATE
     assert L.kv_ipc_export(None, 16, None) == kvr.KV_EINVAL
+
+
+def test_verify_workspace_bytes(L):
+    assert kvr.kv_verify_workspace_bytes(-1, 5) == 0 and kvr.kv_verify_workspace_bytes(2, -1) == 0
+    a = kvr.kv_verify_workspace_bytes(4, 100)
+    b = kvr.kv_verify_workspace_bytes(4, 1000)
+    assert 0 < a < b and b >= 1000 * (8 + 1 + 8)
+    assert kvr.num_entries([0, 1, 16, 17, 33], 16) == 0 + 1 + 1 + 2 + 3
+
+
+def test_verify_rejects_unknown_arena_and_null_records(L):
+    lens, tables = np.array([3, 20], np.int32), np.zeros((2, 2), np.int32)
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_block_digests(0x1234, lens, tables, 0x10000, 1 << 20, 0x2000)
+    assert e.value.status == kvr.KV_ESTATE
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_verify(0x1234, lens, tables, 0, 0x10000, 1 << 20, 0x3000)
+    assert e.value.status == kvr.KV_EINVAL and "committed" in e.value.message
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_verify(0x1234, lens, tables, 0x4000, 0x10000, 1 << 20, 0x3000)
+    assert e.value.status == kvr.KV_ESTATE

@@ -1,0 +1,232 @@
+"""Block commit digests and verification on the GPU (include/kvr_verify.h)
+against the oracle: digests are integer work, so every one must be
+bit-identical to the oracle's; leading-intact counts must equal the oracle's
+on the same damaged arena; and a flush-free recovery (verify, then rebuild
+only the requests that failed) must reproduce the fully rebuilt arena bit for
+bit."""
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from paper_2608_14635_amd import harness as Hn  # noqa: E402
+from paper_2608_14635_amd import kvr  # noqa: E402
+from paper_2608_14635_amd import workloads as W  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+LLAMA8B_2L = W.LLAMA8B.with_layers(2)
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def random_bits(arena: Hn.DeviceArena, seed: int) -> None:
+    """Uniform random raw bits over the whole arena, in chunks, on the device."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    flat = arena.bits.view(-1)
+    lo, hi = (-(1 << 15), 1 << 15) if arena.dt == W.BF16 else (-(1 << 31), 1 << 31)
+    chunk = 1 << 26
+    for i in range(0, flat.numel(), chunk):
+        n = min(chunk, flat.numel() - i)
+        flat[i:i + n] = torch.randint(lo, hi, (n,), generator=g, device="cuda", dtype=flat.dtype)
+
+
+def gpu_digests(arena, wl, lens=None, tables=None):
+    lens = wl.lens if lens is None else lens
+    tables = wl.block_tables if tables is None else tables
+    E = kvr.num_entries(lens, wl.block_size)
+    nbytes = kvr.kv_verify_workspace_bytes(len(lens), E)
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+    out = torch.full((max(E, 1),), -1, dtype=torch.int64, device="cuda")
+    kvr.kv_block_digests(arena.handle, lens, tables, ws.data_ptr(), nbytes, out.data_ptr(),
+                         Hn.stream_ptr())
+    torch.cuda.synchronize()
+    return out[:E].cpu().numpy().view(np.uint64)
+
+
+def gpu_verify(arena, wl, committed: np.ndarray, lens=None, tables=None):
+    lens = wl.lens if lens is None else lens
+    tables = wl.block_tables if tables is None else tables
+    E = kvr.num_entries(lens, wl.block_size)
+    nbytes = kvr.kv_verify_workspace_bytes(len(lens), E)
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+    com = torch.from_numpy(np.ascontiguousarray(committed).view(np.int64).copy()).cuda() if E else \
+        torch.zeros(1, dtype=torch.int64, device="cuda")
+    dg = torch.full((max(E, 1),), -1, dtype=torch.int64, device="cuda")
+    intact = torch.full((max(len(lens), 1),), -5, dtype=torch.int32, device="cuda")
+    kvr.kv_verify(arena.handle, lens, tables, com.data_ptr(), ws.data_ptr(), nbytes,
+                  intact.data_ptr(), dg.data_ptr(), Hn.stream_ptr())
+    torch.cuda.synchronize()
+    return dg[:E].cpu().numpy().view(np.uint64), intact[:len(lens)].cpu().numpy()
+
+
+CASES = {
+    "tiny_f32": (W.TINY_F32, [0, 1, 15, 16, 17, 300, 64], 16),
+    "tiny_bf16_b32": (W.TINY_BF16, [33, 1, 0, 95, 96, 97], 32),
+    "llama8b_2l": (LLAMA8B_2L, [1, 16, 17, 300, 2049, 0, 511], 16),
+    "qwen25_1_5b_2l_b8": (W.QWEN25_1_5B.with_layers(2), [7, 8, 9, 250], 8),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_digests_and_verify_match_oracle(oracle_lib, case):
+    shape, lens, B = CASES[case]
+    wl = W.small_workload(shape, lens, block_size=B, seed=501, other_live_frac=0.3)
+    say(f"digests {case}: lens={lens} B={B} NB={wl.num_blocks}")
+    arena = Hn.DeviceArena(wl)
+    random_bits(arena, seed=77)
+    arena.bind()
+    host = arena.to_host()
+    g = gpu_digests(arena, wl)
+    o, _ = oracle_lib.verify(shape, host, B, wl.num_blocks, wl.lens, wl.block_tables)
+    assert g.size == o.size == kvr.num_entries(wl.lens, B)
+    assert np.array_equal(g, o), f"{int((g != o).sum())} of {g.size} digests differ"
+    nb = (wl.lens + B - 1) // B
+    dg, intact = gpu_verify(arena, wl, o)
+    assert np.array_equal(dg, o) and np.array_equal(intact, nb)
+
+    # damage: one bit of one element in chosen blocks (mirrored on the host copy)
+    signed = host.view(np.int16 if shape.dtype == W.BF16 else np.int32).reshape(arena.shape6)
+    rng = np.random.default_rng(3)
+    damaged = []
+    for r in np.nonzero(nb)[0][::2]:
+        j = int(rng.integers(0, nb[r]))
+        n = min(B, int(wl.lens[r]) - j * B)
+        idx = (int(rng.integers(0, shape.num_layers)), int(rng.integers(0, 2)),
+               int(wl.block_tables[r, j]), int(rng.integers(0, n)),
+               int(rng.integers(0, shape.num_kv_heads)), int(rng.integers(0, shape.head_dim)))
+        signed[idx] ^= 1 << int(rng.integers(0, 15))
+        arena.bits[idx] = int(signed[idx])
+        damaged.append((int(r), j))
+    o2, oi = oracle_lib.verify(shape, host, B, wl.num_blocks, wl.lens, wl.block_tables, o)
+    dg2, intact2 = gpu_verify(arena, wl, o)
+    say(f"  damaged (request, block) {damaged}: intact {intact2.tolist()} of {nb.tolist()}")
+    assert np.array_equal(dg2, o2) and np.array_equal(intact2, oi)
+    for r, j in damaged:
+        assert intact2[r] <= j
+    arena.release()
+
+
+def test_flush_free_recovery_rebuilds_only_damaged_requests(oracle_lib):
+    shape = W.TINY_BF16
+    wl = W.small_workload(shape, [40, 17, 300, 129, 64, 0, 255], seed=511, other_live_frac=0.25)
+    host_w = W.host_weights(shape, seed=512)
+    model = Hn.device_model_from_host(shape, host_w)
+    arena = Hn.DeviceArena(wl, host_image=W.host_arena(wl))
+    arena.bind()
+    T = wl.total_tokens
+    ws, nbytes = Hn.alloc_workspace(shape, wl.num_requests, T, T)
+    say("flush-free recovery: full rebuild, then commit digests")
+    kvr.kv_rebuild(model.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle, ws.data_ptr(),
+                   nbytes, Hn.stream_ptr())
+    committed = gpu_digests(arena, wl)
+    B = wl.block_size
+    # harmless writes: slots past a request's length and free blocks
+    last = wl.block_tables[0, (int(wl.lens[0]) - 1) // B]
+    arena.bits[:, :, last, int(wl.lens[0]) % B:] = 123
+    if wl.other_live.size:
+        arena.bits[0, 1, int(wl.other_live[0])] = -7
+    reference = arena.to_host().copy()
+    # damage: a torn row in request 1's second block, a stale tail block of request 3
+    arena.bits[2, 0, int(wl.block_tables[1, 1]), 0, 1, :64] = 0
+    arena.bits[:, :, int(wl.block_tables[3, 8]), :1] = arena.bits[:, :, int(wl.block_tables[3, 0]), :1].clone()
+    _, intact = gpu_verify(arena, wl, committed)
+    nb = (wl.lens + B - 1) // B
+    _, oi = oracle_lib.verify(shape, arena.to_host(), B, wl.num_blocks, wl.lens, wl.block_tables,
+                              committed)
+    say(f"  intact {intact.tolist()} of {nb.tolist()}")
+    assert np.array_equal(intact, oi)
+    bad = np.nonzero(intact < nb)[0]
+    assert bad.tolist() == [1, 3] and intact[1] == 1 and intact[3] == 8
+    # rebuild the damaged requests only
+    off = wl.request_offsets()
+    toks = np.concatenate([wl.tokens[off[r]:off[r] + wl.lens[r]] for r in bad])
+    kvr.kv_rebuild(model.weights, toks, wl.lens[bad], wl.block_tables[bad], arena.handle,
+                   ws.data_ptr(), nbytes, Hn.stream_ptr())
+    torch.cuda.synchronize()
+    assert np.array_equal(arena.to_host(), reference), "partial recovery differs from the full rebuild"
+    _, intact = gpu_verify(arena, wl, committed)
+    assert np.array_equal(intact, nb)
+    arena.release()
+
+
+def test_verify_argument_errors():
+    shape = W.TINY_F32
+    wl = W.small_workload(shape, [5, 20], seed=521, other_live_frac=0.0)
+    arena = Hn.DeviceArena(wl)
+    arena.bind()
+    ws = torch.empty(1 << 16, dtype=torch.uint8, device="cuda")
+    out = torch.empty(64, dtype=torch.int64, device="cuda")
+    intact = torch.empty(8, dtype=torch.int32, device="cuda")
+    B, tab = wl.block_size, wl.block_tables.copy()
+
+    def status(fn):
+        try:
+            fn()
+            return kvr.KV_OK
+        except kvr.KvError as e:
+            return e.status
+
+    def dig(lens, tables, nbytes=1 << 16):
+        return status(lambda: kvr.kv_block_digests(arena.handle, lens, tables, ws.data_ptr(), nbytes,
+                                                   out.data_ptr()))
+    assert dig(wl.lens, tab) == kvr.KV_OK
+    assert dig([5, -1], tab) == kvr.KV_EINVAL
+    assert dig([5, B * tab.shape[1] + 1], tab) == kvr.KV_ECAPACITY
+    bad = tab.copy()
+    bad[1, 1] = wl.num_blocks
+    assert dig(wl.lens, bad) == kvr.KV_ERANGE
+    bad[1, 1] = -1
+    assert dig(wl.lens, bad) == kvr.KV_ERANGE
+    bad = tab.copy()
+    bad[0, 1] = 10 ** 6            # past request 0's blocks: never read
+    assert dig(wl.lens, bad) == kvr.KV_OK
+    assert dig(wl.lens, tab, nbytes=64) == kvr.KV_ENOMEM
+    assert dig(np.zeros(0, np.int32), np.zeros((0, 0), np.int32), nbytes=0) == kvr.KV_OK
+    # all-empty requests: intact counts are 0 = their block counts
+    com = torch.zeros(4, dtype=torch.int64, device="cuda")
+    intact.fill_(-1)
+    kvr.kv_verify(arena.handle, [0, 0], tab, com.data_ptr(), ws.data_ptr(), 1 << 16, intact.data_ptr())
+    torch.cuda.synchronize()
+    assert intact[:2].tolist() == [0, 0]
+    arena.release()
+
+
+def test_digests_full_size_sampled(oracle_lib):
+    """The Llama-3-8B rebuild workload at full size (16 requests, 128K tokens,
+    33.7 GB arena) in the launch configuration the benchmark times: every
+    entry digested on the GPU, a sample checked against the oracle block by
+    block (each block copied into a one-block arena of the same geometry)."""
+    wl = W.config2()
+    s, B = wl.shape, wl.block_size
+    say(f"full-size digests: {wl.num_requests} requests, {wl.total_tokens} tokens, "
+        f"{wl.num_blocks} blocks")
+    arena = Hn.DeviceArena(wl)
+    random_bits(arena, seed=91)
+    arena.bind()
+    g = gpu_digests(arena, wl)
+    nb = (wl.lens + B - 1) // B
+    assert g.size == int(nb.sum())
+    entries = [(r, j) for r in range(wl.num_requests) for j in range(int(nb[r]))]
+    rng = np.random.default_rng(17)
+    pick = sorted(set(rng.choice(len(entries), size=40, replace=False).tolist())
+                  | {0, len(entries) - 1} | {int(np.cumsum(nb)[r]) - 1 for r in range(wl.num_requests)})
+    el = np.uint16 if s.dtype == W.BF16 else np.uint32
+    for e in pick:
+        r, j = entries[e]
+        n = min(B, int(wl.lens[r]) - j * B)
+        blk = int(wl.block_tables[r, j])
+        mini = np.ascontiguousarray(arena.bits[:, :, blk].cpu().numpy()).view(el).reshape(-1)
+        want = oracle_lib.block_digest(s, mini, B, 1, 0, n)
+        assert int(g[e]) == want, (e, r, j, n)
+    assert len(set(g.tolist())) == g.size, "distinct random blocks gave equal digests"
+    say(f"  {len(pick)} sampled entries match the oracle; {g.size} distinct digests")
+    arena.release()
+    del arena
+    torch.cuda.empty_cache()
