@@ -35,6 +35,7 @@ KERNEL_SOURCES = {
     "gemm_gateup": ["gemm_bf16.hip", "epilogue.h", "common.h", "launch.h"],
     "gemm_down": ["gemm_bf16.hip", "epilogue.h", "common.h", "launch.h"],
     "attention": ["attention.hip", "common.h", "launch.h"],
+    "verify": ["verify.hip", "launch.h"],
 }
 
 
@@ -166,6 +167,7 @@ def flush_free(wl, model, arena, ws_rebuild, Hn, kvr, reps, stream, log):
     healed = bool(np.array_equal(intact[:R].cpu().numpy(), nb))
     out = {"entries": E, "verify_ms": ms, "covered_bytes": covered, "bytes_per_launch": moved,
            "achieved_GBps": moved / (ms / 1e3) / 1e9, "hbm_frac": moved / (ms / 1e3) / 1e9 / PEAK_HBM_GBS,
+           "traffic": measured_traffic("verify", wl.name), "source_sha": kernel_source_hash("verify"),
            "all_intact_after_rebuild": all_intact,
            "one_damaged_request": {"request": r, "tokens": int(wl.lens[r]),
                                    "detected": bad.tolist(), "recovery_ms": rec_ms,
@@ -362,13 +364,16 @@ def main():
     gemm_ms = sum(prof[k]["ms"] for k in gemm_keys)
     gemm_tf = sum(prof[k]["flops"] for k in gemm_keys) / (gemm_ms / 1e3) / 1e12 if gemm_ms else 0.0
 
-    dec = None
-    if args.decode_steps > 0 and wl.num_requests > 0:
-        dec = resume_decode(wl, model, arena, Hn, kvr, W, args.decode_steps, stream, log)
-
+    # the verification runs over the rebuilt arena before resumed decode
+    # rewrites each request's last slot (decode rounds differently from the
+    # prefill, so its rows would need commit records of their own)
     ff = None
     if args.verify_reps > 0 and wl.num_requests > 0:
         ff = flush_free(wl, model, arena, (ws, nbytes), Hn, kvr, args.verify_reps, stream, log)
+
+    dec = None
+    if args.decode_steps > 0 and wl.num_requests > 0:
+        dec = resume_decode(wl, model, arena, Hn, kvr, W, args.decode_steps, stream, log)
 
     cpu = None
     if not args.no_cpu_baseline:
