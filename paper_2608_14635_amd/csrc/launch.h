@@ -67,6 +67,7 @@ struct GemmParams {
   float* part;
   int64_t part_stride;
   int part_ld;
+  int group_m;            // M tiles walked together by an XCD's workgroups (set by the launcher)
 };
 
 // Elementwise / small kernels
