@@ -13,7 +13,8 @@
 // operand.  K rows are placed in LDS with bits 2 and 3 of their index swapped,
 // which makes the 8 keys of each P^T operand slot group contiguous in V^T, so
 // every V^T operand is one 16-byte LDS read.  exp2 with the scale folded in;
-// P rounded to bf16 for the MFMA; fp32 accumulation; masking only on tiles
+// P rounded to bf16 for the MFMA, and the softmax denominator summed from
+// the same rounded values (bf16 dot2 with fp32 accumulation); fp32 accumulation; masking only on tiles
 // that cross a wave's diagonal; the O rescale runs only when some lane's
 // max rose by a factor above 2^8 since the last one.  q-blocks are
 // scheduled longest-first.  Deterministic: fixed key order, no atomics.
@@ -219,17 +220,24 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
         m_run = m_new;
       }
       const float neg_m = -m_run;
-      float lsum = 0.0f;
       bf16x8 pf[4];
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float e = __builtin_amdgcn_exp2f(fmaf(s[k2][r], scale_log2, neg_m));
-          lsum += e;
-          pf[k2 * 2 + (r >> 3)][r & 7] = (__bf16)e;
-        }
-      l_run += lsum;
+        for (int r = 0; r < 16; ++r)
+          pf[k2 * 2 + (r >> 3)][r & 7] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[k2][r], scale_log2, neg_m));
+      // row sums of the rounded P (exactly the weights the PV MFMA applies),
+      // two values per instruction
+      float lsum0 = 0.0f, lsum1 = 0.0f;
+      const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        lsum0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[c], pf[c], 0, 1), one2, lsum0, false);
+        lsum1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[c], pf[c], 2, 3), one2, lsum1, false);
+        lsum0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[c], pf[c], 4, 5), one2, lsum0, false);
+        lsum1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[c], pf[c], 6, 7), one2, lsum1, false);
+      }
+      l_run += lsum0 + lsum1;
       // ---- O^T += V^T P^T; P^T slot j of chunk c is key 16c + 8*half + j (the
       // four d-tiles' chains alternate) ----
 #pragma unroll
