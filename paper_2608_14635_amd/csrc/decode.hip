@@ -15,7 +15,10 @@
 // wave owns a head's running max and sum), and accumulates P.V with threads
 // over (head, dim).  Each split writes (m, l, o[d]) partials; a second kernel
 // merges the splits in index order, so results do not depend on timing.
-// The step is HBM-bound on the context's K/V reads.
+// The step is HBM-bound on the context's K/V reads.  For bf16 models with
+// head_dim 128 a second kernel does the same work with matrix-core scores
+// and register-direct loads (decode_attn_mfma_kernel); the general one
+// serves fp32 models and other head sizes.
 #include <algorithm>
 
 #include "common.h"
@@ -30,6 +33,7 @@ constexpr int DNT = 256;   // 4 waves
 constexpr int DMAXG = 16;  // q heads per kv head supported
 constexpr int DMAXD = 128;
 constexpr int TABN = 1024;  // block-table entries staged in LDS per workgroup
+constexpr int DMAXS = 128;  // key ranges per (request, kv head) the combine supports
 
 __global__ void rope_rows_kernel(float2* table, const int32_t* positions, int rows, int half,
                                  double theta, int d) {
@@ -209,19 +213,210 @@ __global__ __launch_bounds__(DNT) void decode_attn_kernel(DecodeAttnParams p) {
   }
 }
 
+// bf16, head_dim 128: one wave per (request, kv head, key range) over tiles
+// of 16 keys (a tile never crosses an arena block when the block size is a
+// multiple of 16).  Each lane loads 16-byte pieces of the keys' K and V rows
+// straight into registers (a key's 256-byte head slice is four lanes' worth
+// per instruction), and the next tile is in flight while this one is used.
+// Scores: S^T = K Q^T on v_mfma_f32_16x16x32_bf16 with the g q heads as the
+// 16 columns (unused columns hold zero queries): lane (q, c) = (lane/16,
+// lane%16) gets keys 4q..4q+3 of head c.  Online softmax per head in the exp2
+// domain, rescaling only when a head's max rose by more than 2^DSLACK.  P.V in
+// fp32 on the VALU: lane (q, c) owns dims 8c..8c+7 of keys 4q..4q+3 and
+// reads every head's P of those keys from its wave's LDS area; the four lane
+// groups' partial sums are added at the end.  Same (o, m, l) partials as the
+// general kernel.
+constexpr int DT = 16;           // keys per tile
+constexpr float DSLACK = 8.0f;   // rescale slack, log2 units
+
+template <int GM>
+__global__ __launch_bounds__(256) void decode_attn_mfma_kernel(DecodeAttnParams p) {
+  __shared__ __attribute__((aligned(16))) float s_p[4][GM * DT];
+  __shared__ float s_a[4][16];
+  const int S = p.splits, ngrp = (p.nkv + 3) / 4;
+  int bid = blockIdx.x;
+  const int split = bid % S;
+  bid /= S;
+  const int kgrp = bid % ngrp, r = bid / ngrp;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int kvh = kgrp * 4 + wave;
+  if (kvh >= p.nkv) return;  // whole waves
+  const int g = p.nq / p.nkv;
+  const int c = lane & 15, q = lane >> 4;
+  const int ctx = p.ctx[r];
+  const int chunk = ((ctx + S - 1) / S + DT - 1) / DT * DT;
+  const int k0 = split * chunk, k1 = min(ctx, k0 + chunk);
+  const float scale_log2 = 1.4426950408889634f / sqrtf(128.0f);
+  const int64_t row_bytes = (int64_t)p.nkv * 128 * 2;
+  const char* Kb = reinterpret_cast<const char*>(p.plane_k) + kvh * 256;
+  const char* Vb = reinterpret_cast<const char*>(p.plane_v) + kvh * 256;
+  const int* table = p.tables + (int64_t)r * p.max_blocks;
+  const int B = p.block_size;
+
+  // Q^T operand: head c (zero past g), dims 32t + 8q .. +7
+  bf16x8 qf[4];
+  {
+    const bf16_t* qrow = reinterpret_cast<const bf16_t*>(p.q) +
+                         ((int64_t)r * p.nq + kvh * g + min(c, g - 1)) * 128 + 8 * q;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      qf[t] = *reinterpret_cast<const bf16x8*>(qrow + 32 * t);
+      if (c >= g) qf[t] = bf16x8{};
+    }
+  }
+  float m_run = -INFINITY, l_run = 0.0f;
+  float o[GM][8];
+#pragma unroll
+  for (int h = 0; h < GM; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[h][e] = 0.0f;
+  float* sp = s_p[wave];
+
+  auto load = [&](int kb, bf16x8* kr, bf16x8* vr) {
+    const int64_t row0 = (int64_t)table[kb / B] * B + kb % B;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      kr[t] = *reinterpret_cast<const bf16x8*>(Kb + (row0 + c) * row_bytes + (32 * t + 8 * q) * 2);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      vr[i] = *reinterpret_cast<const bf16x8*>(Vb + (row0 + 4 * q + i) * row_bytes + c * 16);
+  };
+  bf16x8 kf[4], vf[4];
+  if (k0 < k1) load(k0, kf, vf);
+  for (int kb = k0; kb < k1; kb += DT) {
+    bf16x8 kn[4], vn[4];
+    if (kb + DT < k1) load(kb + DT, kn, vn);
+    f32x4 st = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[t], qf[t], st, 0, 0, 0);
+    // scores of keys 4q+j for head c; keys past the range are masked and
+    // their V rows (which may hold any bits) zeroed
+    float sc[4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool ok = kb + 4 * q + j < k1;
+      sc[j] = ok ? st[j] * scale_log2 : -INFINITY;
+      if (!ok) vf[j] = bf16x8{};
+      mx = fmaxf(mx, sc[j]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    if (__any(mx > m_run + DSLACK)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+      m_run = m_new;
+      if (q == 0) s_a[wave][c] = alpha;
+#pragma unroll
+      for (int h = 0; h < GM; ++h) {
+        const float a = s_a[wave][h];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[h][e] *= a;
+      }
+    }
+    float pr[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      pr[j] = __builtin_amdgcn_exp2f(sc[j] - m_run);
+      l_run += pr[j];
+    }
+    if (c < GM) *reinterpret_cast<float4*>(sp + c * DT + 4 * q) = make_float4(pr[0], pr[1], pr[2], pr[3]);
+    float4 ph[GM];
+#pragma unroll
+    for (int h = 0; h < GM; ++h) ph[h] = *reinterpret_cast<const float4*>(sp + h * DT + 4 * q);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float v[8];
+      const uint4 u = __builtin_bit_cast(uint4, vf[i]);
+      v[0] = __uint_as_float(u.x << 16); v[1] = __uint_as_float(u.x & 0xffff0000u);
+      v[2] = __uint_as_float(u.y << 16); v[3] = __uint_as_float(u.y & 0xffff0000u);
+      v[4] = __uint_as_float(u.z << 16); v[5] = __uint_as_float(u.z & 0xffff0000u);
+      v[6] = __uint_as_float(u.w << 16); v[7] = __uint_as_float(u.w & 0xffff0000u);
+#pragma unroll
+      for (int h = 0; h < GM; ++h) {
+        if (h < g) {
+          const float w = i == 0 ? ph[h].x : i == 1 ? ph[h].y : i == 2 ? ph[h].z : ph[h].w;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[h][e] = fmaf(w, v[e], o[h][e]);
+        }
+      }
+    }
+    if (kb + DT < k1) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        kf[t] = kn[t];
+        vf[t] = vn[t];
+      }
+    }
+  }
+  // the four lane groups' sums; lanes of group 0 write head h's dims 8c..8c+7
+  // and head c's (m, l)
+  float l = l_run + __shfl_xor(l_run, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+#pragma unroll
+  for (int h = 0; h < GM; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      o[h][e] += __shfl_xor(o[h][e], 16, 64);
+      o[h][e] += __shfl_xor(o[h][e], 32, 64);
+    }
+  if (q != 0) return;
+  const int stride = 128 + 2;
+#pragma unroll
+  for (int h = 0; h < GM; ++h) {
+    if (h < g) {
+      float* dst = p.part + (((int64_t)r * p.nq + kvh * g + h) * S + split) * stride + 8 * c;
+      *reinterpret_cast<float4*>(dst) = make_float4(o[h][0], o[h][1], o[h][2], o[h][3]);
+      *reinterpret_cast<float4*>(dst + 4) = make_float4(o[h][4], o[h][5], o[h][6], o[h][7]);
+    }
+  }
+  if (c < g) {
+    float* tail = p.part + (((int64_t)r * p.nq + kvh * g + c) * S + split) * stride + 128;
+    tail[0] = m_run;
+    tail[1] = l;
+  }
+}
+
 // Merge the splits of one (request, q head) in split order; round to T.
+// The splits' weights exp2(m_s - M) are formed once (thread s) and shared
+// through LDS; every output dim then sums its splits in index order.
 template <typename T>
 __global__ __launch_bounds__(DMAXD) void decode_combine_kernel(DecodeAttnParams p) {
+  __shared__ float s_w[DMAXS], s_red[DMAXD];
   const int r = blockIdx.x / p.nq, h = blockIdx.x % p.nq;
   const int e = threadIdx.x, d = p.d, S = p.splits, stride = d + 2;
   const float* base = p.part + ((int64_t)r * p.nq + h) * S * stride;
-  float M = -INFINITY;
-  for (int s = 0; s < S; ++s) M = fmaxf(M, base[s * stride + d]);
+  // M: maximum of the splits' m (order-free)
+  float mloc = -INFINITY;
+  for (int s = e; s < S; s += DMAXD) mloc = fmaxf(mloc, base[s * stride + d]);
+  s_red[e] = mloc;
+  __syncthreads();
+  for (int w = DMAXD / 2; w > 0; w >>= 1) {
+    if (e < w) s_red[e] = fmaxf(s_red[e], s_red[e + w]);
+    __syncthreads();
+  }
+  const float M = s_red[0];
+  for (int s = e; s < S; s += DMAXD) s_w[s] = __builtin_amdgcn_exp2f(base[s * stride + d] - M);
+  __syncthreads();
   float L = 0.0f, o = 0.0f;
-  for (int s = 0; s < S; ++s) {
-    const float w = __builtin_amdgcn_exp2f(base[s * stride + d] - M);
-    L = fmaf(base[s * stride + d + 1], w, L);
-    if (e < d) o = fmaf(base[s * stride + e], w, o);
+  int s = 0;
+  for (; s + 4 <= S; s += 4) {
+    float v[4], l[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      l[u] = base[(s + u) * stride + d + 1];
+      v[u] = e < d ? base[(s + u) * stride + e] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      L = fmaf(l[u], s_w[s + u], L);
+      o = fmaf(v[u], s_w[s + u], o);
+    }
+  }
+  for (; s < S; ++s) {
+    L = fmaf(base[s * stride + d + 1], s_w[s], L);
+    if (e < d) o = fmaf(base[s * stride + e], s_w[s], o);
   }
   if (e < d) {
     T* out = reinterpret_cast<T*>(p.out) + (int64_t)r * p.nq * d + (int64_t)h * d;
@@ -285,12 +480,13 @@ void launch_rope_rows(float2* table, const int32_t* positions, int rows, int d, 
 }
 
 int decode_attn_splits(int num_requests, int nkv, int64_t max_ctx) {
-  // about 2048 workgroups in all, at least 256 keys and at most 64 splits per
-  // (request, kv head); never more for more requests, so a workspace sized
-  // for one request's split count fits any larger batch
+  // about 8192 (request, kv head, key range) items in all, at least 64 keys
+  // and at most 128 ranges per (request, kv head); never more for more
+  // requests, so a workspace sized for one request's split count fits any
+  // larger batch
   const int64_t pairs = std::max<int64_t>(1, (int64_t)num_requests * nkv);
-  const int64_t want = (2048 + pairs - 1) / pairs;
-  const int64_t cap = std::min<int64_t>(64, (max_ctx + 255) / 256);
+  const int64_t want = (8192 + pairs - 1) / pairs;
+  const int64_t cap = std::min<int64_t>(DMAXS, (max_ctx + 63) / 64);
   return (int)std::max<int64_t>(1, std::min(want, cap));
 }
 
@@ -299,7 +495,17 @@ void launch_decode_attention(int dtype, const DecodeAttnParams& p, int num_reque
   if (num_requests <= 0) return;
   const dim3 grid((unsigned)((int64_t)num_requests * p.nkv * p.splits));
   const dim3 cgrid((unsigned)((int64_t)num_requests * p.nq));
-  if (dtype == 1) {
+  const int g = p.nq / p.nkv;
+  if (dtype == 1 && p.d == 128 && p.block_size % DT == 0 && g <= 16) {
+    const dim3 mgrid((unsigned)((int64_t)num_requests * ((p.nkv + 3) / 4) * p.splits));
+    if (g <= 4)
+      hipLaunchKernelGGL(decode_attn_mfma_kernel<4>, mgrid, dim3(256), 0, s, p);
+    else if (g <= 8)
+      hipLaunchKernelGGL(decode_attn_mfma_kernel<8>, mgrid, dim3(256), 0, s, p);
+    else
+      hipLaunchKernelGGL(decode_attn_mfma_kernel<16>, mgrid, dim3(256), 0, s, p);
+    hipLaunchKernelGGL(decode_combine_kernel<bf16_t>, cgrid, dim3(DMAXD), 0, s, p);
+  } else if (dtype == 1) {
     hipLaunchKernelGGL(decode_attn_kernel<bf16_t>, grid, dim3(DNT), 0, s, p);
     hipLaunchKernelGGL(decode_combine_kernel<bf16_t>, cgrid, dim3(DMAXD), 0, s, p);
   } else {

@@ -395,25 +395,9 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
   }
 }
 
-// Split-K partials summed in split order into slice 0 (one float4 per
-// thread, all outputs in parallel), then the fused epilogue on slice 0 in
-// 32-row x 256-column pieces, exactly as the one-pass GEMM would apply it.
-__global__ __launch_bounds__(256) void splitk_sum_kernel(float* part, int64_t n4, int ksplit,
-                                                         int64_t stride) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= n4) return;
-  float4* p0 = reinterpret_cast<float4*>(part) + i;
-  float4 a = *p0;
-  for (int sp = 1; sp < ksplit; ++sp) {
-    const float4 v = *(reinterpret_cast<const float4*>(part + sp * stride) + i);
-    a.x += v.x;
-    a.y += v.y;
-    a.z += v.z;
-    a.w += v.w;
-  }
-  *p0 = a;
-}
-
+// Split-K partials summed in split order (slice 0, then += slice 1, ...),
+// then the fused epilogue, in 32-row x 256-column pieces, exactly as the
+// one-pass GEMM would apply it.
 constexpr int SK_ROWS = 32;
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_epi_kernel(GemmParams p, int tiles_n) {
@@ -424,7 +408,17 @@ __global__ __launch_bounds__(256) void splitk_epi_kernel(GemmParams p, int tiles
     const int r = it / (BN / 4), c = (it % (BN / 4)) * 4;
     const int m = m0 + r;
     float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if (m < p.M) a = *reinterpret_cast<const float4*>(p.part + (int64_t)m * p.part_ld + tile_n * BN + c);
+    if (m < p.M) {
+      const float* src = p.part + (int64_t)m * p.part_ld + tile_n * BN + c;
+      a = *reinterpret_cast<const float4*>(src);
+      for (int sp = 1; sp < p.ksplit; ++sp) {
+        const float4 v = *reinterpret_cast<const float4*>(src + sp * p.part_stride);
+        a.x += v.x;
+        a.y += v.y;
+        a.z += v.z;
+        a.w += v.w;
+      }
+    }
     *reinterpret_cast<float4*>(sC + r * LDC + c) = a;
   }
   __syncthreads();
@@ -437,6 +431,129 @@ __global__ __launch_bounds__(256) void splitk_epi_kernel(GemmParams p, int tiles
   } else {
     epi_swiglu<bf16_t, BN, 256>(sC, LDC, SK_ROWS, m0, p.M, tile_n * (BN / 2), p.epi);
   }
+}
+
+// ---- products of few rows (resumed decode) ----
+// C[M <= 64, N] = A . B^T, weight-stationary: each wave owns 16 output columns
+// (16 weight rows) and one K range, streams those rows once with 16-byte
+// loads (per 128-k chunk a lane takes 64 contiguous bytes of its row) and
+// multiplies them with every row of A on v_mfma_f32_16x16x32_bf16 (16-row
+// tiles of A; rows past M are clamped and their results dropped).  No LDS
+// and no padding work: HBM-bound on the weights, while A stays in L2.  The
+// weight loads are plain (cached): a load instruction covers 64 bytes of
+// each of 16 rows, and the next one the rest of those lines, which
+// nontemporal loads would fetch again.  In a
+// chunk, MFMA t takes from lane group q = lane/16 the k values 32q+8t..+7 of
+// both operands, a fixed partition of the chunk's 128 k.  Output: the fp32
+// partial sums of the K range, in the split-K partial layout.
+constexpr int SK_CHUNK = 128;   // k per chunk
+constexpr int SK_UNROLL = 4;    // chunks in flight per wave
+constexpr int SK_MAX_M = 64;
+// waves a launch aims for (K is split to get there): fewer, longer waves for
+// the narrow products, more for the wide ones (measured best on the 8B shapes)
+constexpr int SK_WAVES_NARROW = 2048, SK_WAVES_WIDE = 8192, SK_NARROW_BLOCKS = 512;
+
+template <int MT>
+__global__ __launch_bounds__(256) void gemm_bf16_skinny_kernel(GemmParams p, int nblocks, int kc_per) {
+  const int lane = threadIdx.x & 63;
+  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (item >= nblocks * p.ksplit) return;  // whole waves
+  const int nb = item / p.ksplit, split = item % p.ksplit;
+  const int tile_n = nb / (BN / 16), c0 = (nb % (BN / 16)) * 16;
+  const int r16 = lane & 15, q = lane >> 4;
+  const bf16_t* brow = b_row_ptr(p, tile_n, c0 + r16) + 32 * q;
+  const bf16_t* arow[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+    arow[mt] = reinterpret_cast<const bf16_t*>(p.A) + (int64_t)min(mt * 16 + r16, p.M - 1) * p.lda + 32 * q;
+  const int KC = p.K / SK_CHUNK;
+  const int kc0 = split * kc_per, kc1 = min(KC, kc0 + kc_per);
+  f32x4 acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int kc = kc0; kc < kc1; kc += SK_UNROLL) {
+    bf16x8 bv[SK_UNROLL][4], av[SK_UNROLL][MT][4];
+#pragma unroll
+    for (int u = 0; u < SK_UNROLL; ++u) {
+      if (kc + u < kc1) {
+        const int ko = (kc + u) * SK_CHUNK;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          bv[u][t] = *reinterpret_cast<const bf16x8*>(brow + ko + 8 * t);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) av[u][mt][t] = *reinterpret_cast<const bf16x8*>(arow[mt] + ko + 8 * t);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < SK_UNROLL; ++u) {
+      if (kc + u < kc1) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u][mt][t], bv[u][t], acc[mt], 0, 0, 0);
+      }
+    }
+  }
+  // a lane holds rows 4q .. 4q+3 of each 16-row tile, at column c0 + r16
+  float* out = p.part + split * p.part_stride + tile_n * BN + c0 + r16;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int m = mt * 16 + 4 * q + j;
+      if (m < p.M) out[(int64_t)m * p.part_ld] = acc[mt][j];
+    }
+}
+
+// Elementwise epilogues (residual add, store) of a split-K product: one
+// float4 of the output per thread, the splits summed in index order exactly
+// as splitk_epi_kernel sums them, so every output is parallel work.
+template <int EPI>
+__global__ __launch_bounds__(256) void splitk_elem_kernel(GemmParams p) {
+  const int ld4 = p.part_ld / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)p.M * ld4) return;
+  const int m = (int)(i / ld4), col = (int)(i % ld4) * 4;
+  const float* src = p.part + (int64_t)m * p.part_ld + col;
+  float4 a = *reinterpret_cast<const float4*>(src);
+  for (int sp = 1; sp < p.ksplit; ++sp) {
+    const float4 v = *reinterpret_cast<const float4*>(src + sp * p.part_stride);
+    a.x += v.x;
+    a.y += v.y;
+    a.z += v.z;
+    a.w += v.w;
+  }
+  float4* xp = reinterpret_cast<float4*>(p.epi.x + (int64_t)m * p.epi.ldx + p.n_begin + col);
+  if (EPI == EPI_RESID) {
+    float4 xv = *xp;
+    xv.x += a.x;
+    xv.y += a.y;
+    xv.z += a.z;
+    xv.w += a.w;
+    *xp = xv;
+  } else {
+    *xp = a;
+  }
+}
+
+struct SkinnyPlan {
+  int nblocks, ksplit, kc_per;
+};
+
+bool skinny_ok(int M, int K) { return M > 0 && M <= SK_MAX_M && K % SK_CHUNK == 0; }
+
+SkinnyPlan skinny_plan(int tiles_n, int K) {
+  SkinnyPlan sp;
+  sp.nblocks = tiles_n * (BN / 16);
+  const int KC = K / SK_CHUNK;
+  const int waves = sp.nblocks <= SK_NARROW_BLOCKS ? SK_WAVES_NARROW : SK_WAVES_WIDE;
+  const int want = std::max(1, std::min(KC, (waves + sp.nblocks - 1) / std::max(1, sp.nblocks)));
+  sp.kc_per = (KC + want - 1) / want;
+  sp.ksplit = (KC + sp.kc_per - 1) / sp.kc_per;
+  return sp;
 }
 
 struct SplitPlan {
@@ -464,6 +581,7 @@ int group_m_for(int tiles_n) { return tiles_n <= 16 ? 4 : 8; }
 }  // namespace
 
 int64_t gemm_bf16_splitk_part_elems(int M, int N, int K) {
+  if (skinny_ok(M, K)) return (int64_t)skinny_plan(N / BN, K).ksplit * M * (N / BN) * BN;
   const SplitPlan sp = split_plan(M, N / BN, K);
   return (int64_t)sp.ksplit * M * sp.tiles_n * BN;
 }
@@ -473,33 +591,44 @@ void launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s);
 void launch_gemm_bf16_splitk(int epi, const GemmParams& p, float* part, int64_t part_cap,
                              hipStream_t s) {
   if (p.M <= 0) return;
-  const SplitPlan sp = split_plan(p.M, n_tiles_of(p), p.K);
-  const int64_t ld = (int64_t)sp.tiles_n * BN;
-  if (sp.ksplit <= 1 || (int64_t)sp.ksplit * p.M * ld > part_cap) {
-    launch_gemm_bf16(epi, p, s);
-    return;
-  }
+  const int tiles_n = n_tiles_of(p);
+  const int64_t ld = (int64_t)tiles_n * BN;
   GemmParams q = p;
-  q.group_m = group_m_for(sp.tiles_n);
-  q.ksplit = sp.ksplit;
-  q.kt_per = sp.kt_per;
   q.part = part;
   q.part_ld = (int)ld;
   q.part_stride = (int64_t)p.M * ld;
-  const dim3 grid((unsigned)(sp.tiles_m * sp.tiles_n * sp.ksplit)), block(NT);
-  hipLaunchKernelGGL(gemm_bf16_kernel<EPI_PARTIAL>, grid, block, 0, s, q, sp.tiles_m, sp.tiles_n);
-  const int64_t n4 = q.part_stride / 4;
-  hipLaunchKernelGGL(splitk_sum_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, part, n4,
-                     sp.ksplit, q.part_stride);
-  const dim3 egrid((unsigned)(((p.M + SK_ROWS - 1) / SK_ROWS) * sp.tiles_n));
+  if (skinny_ok(p.M, p.K) && (int64_t)skinny_plan(tiles_n, p.K).ksplit * p.M * ld <= part_cap) {
+    const SkinnyPlan kp = skinny_plan(tiles_n, p.K);
+    q.ksplit = kp.ksplit;
+    const dim3 grid((unsigned)((kp.nblocks * kp.ksplit + 3) / 4)), block(256);
+    switch ((p.M + 15) / 16) {
+      case 1: hipLaunchKernelGGL(gemm_bf16_skinny_kernel<1>, grid, block, 0, s, q, kp.nblocks, kp.kc_per); break;
+      case 2: hipLaunchKernelGGL(gemm_bf16_skinny_kernel<2>, grid, block, 0, s, q, kp.nblocks, kp.kc_per); break;
+      case 3: hipLaunchKernelGGL(gemm_bf16_skinny_kernel<3>, grid, block, 0, s, q, kp.nblocks, kp.kc_per); break;
+      default: hipLaunchKernelGGL(gemm_bf16_skinny_kernel<4>, grid, block, 0, s, q, kp.nblocks, kp.kc_per); break;
+    }
+  } else {
+    const SplitPlan sp = split_plan(p.M, tiles_n, p.K);
+    if (sp.ksplit <= 1 || (int64_t)sp.ksplit * p.M * ld > part_cap) {
+      launch_gemm_bf16(epi, p, s);
+      return;
+    }
+    q.group_m = group_m_for(sp.tiles_n);
+    q.ksplit = sp.ksplit;
+    q.kt_per = sp.kt_per;
+    const dim3 grid((unsigned)(sp.tiles_m * sp.tiles_n * sp.ksplit)), block(NT);
+    hipLaunchKernelGGL(gemm_bf16_kernel<EPI_PARTIAL>, grid, block, 0, s, q, sp.tiles_m, sp.tiles_n);
+  }
+  const dim3 egrid((unsigned)(((p.M + SK_ROWS - 1) / SK_ROWS) * tiles_n));
+  const dim3 lgrid((unsigned)(((int64_t)p.M * (ld / 4) + 255) / 256));
   if (epi == EPI_QKV)
-    hipLaunchKernelGGL(splitk_epi_kernel<EPI_QKV>, egrid, dim3(256), 0, s, q, sp.tiles_n);
+    hipLaunchKernelGGL(splitk_epi_kernel<EPI_QKV>, egrid, dim3(256), 0, s, q, tiles_n);
   else if (epi == EPI_RESID)
-    hipLaunchKernelGGL(splitk_epi_kernel<EPI_RESID>, egrid, dim3(256), 0, s, q, sp.tiles_n);
+    hipLaunchKernelGGL(splitk_elem_kernel<EPI_RESID>, lgrid, dim3(256), 0, s, q);
   else if (epi == EPI_STORE)
-    hipLaunchKernelGGL(splitk_epi_kernel<EPI_STORE>, egrid, dim3(256), 0, s, q, sp.tiles_n);
+    hipLaunchKernelGGL(splitk_elem_kernel<EPI_STORE>, lgrid, dim3(256), 0, s, q);
   else
-    hipLaunchKernelGGL(splitk_epi_kernel<EPI_SWIGLU>, egrid, dim3(256), 0, s, q, sp.tiles_n);
+    hipLaunchKernelGGL(splitk_epi_kernel<EPI_SWIGLU>, egrid, dim3(256), 0, s, q, tiles_n);
 }
 
 void launch_gemm_bf16(int epi, const GemmParams& p_in, hipStream_t s) {
