@@ -32,7 +32,16 @@ SHAPES = {
     "llama8b_2l": dataclasses.replace(W.LLAMA8B.with_layers(2), vocab=2048),
     # the paper's model family: per-head q/k RMSNorm
     "qwen3_8b_2l": dataclasses.replace(W.QWEN3_8B.with_layers(2), vocab=2048),
+    # 6 q heads per kv head, q/k/v bias (Qwen2.5 widths)
+    "qwen25_1_5b_2l": dataclasses.replace(W.QWEN25_1_5B.with_layers(2), vocab=2048),
+    # 16 q heads per kv head
+    "g16_bf16": dataclasses.replace(W.TINY_BF16, num_q_heads=32, num_kv_heads=2),
 }
+# (shape, prefix lengths, block size): the default cases plus block size 32
+# and a batch of 40 requests (three 16-row tiles in the few-row products)
+CASES = {n: (n, None, 16) for n in SHAPES}
+CASES["tiny_bf16_b32"] = ("tiny_bf16", [1, 31, 32, 33, 97], 32)
+CASES["tiny_bf16_40req"] = ("tiny_bf16", [1 + (7 * i) % 90 for i in range(40)], 16)
 
 
 def say(msg):
@@ -40,9 +49,10 @@ def say(msg):
     sys.stdout.flush()
 
 
-def resume_workload(shape, prefix_lens, steps, seed):
+def resume_workload(shape, prefix_lens, steps, seed, block_size=16):
     """Block tables sized for prefix + steps tokens; tokens and lens hold the prefixes."""
-    wl = W.small_workload(shape, [n + steps for n in prefix_lens], seed=seed, other_live_frac=0.25)
+    wl = W.small_workload(shape, [n + steps for n in prefix_lens], block_size=block_size, seed=seed,
+                          other_live_frac=0.25)
     offs = wl.request_offsets()
     toks = np.concatenate([wl.tokens[offs[r]:offs[r] + prefix_lens[r]] for r in range(len(prefix_lens))])
     return dataclasses.replace(wl, lens=np.array(prefix_lens, dtype=wl.lens.dtype), tokens=toks)
@@ -97,14 +107,16 @@ def assert_valid_argmax(gpu_tok, ora_logits, tol):
         assert z[t] >= z.max() - tol * np.max(np.abs(z)), (r, t, int(np.argmax(z)), z[t], z.max())
 
 
-@pytest.mark.parametrize("name", list(SHAPES))
+@pytest.mark.parametrize("name", list(CASES))
 def test_decode_step_matches_oracle(oracle_lib, name):
-    shape = SHAPES[name]
+    sname, prefix, B = CASES[name]
+    shape = SHAPES[sname]
     tol = PU.TOL[shape.dtype]
-    prefix = [1, 6, 23, 300] if name != "tiny_f32" else [1, 6, 23, 100]
-    wl = resume_workload(shape, prefix, steps=2, seed=201)
+    if prefix is None:
+        prefix = [1, 6, 23, 300] if sname != "tiny_f32" else [1, 6, 23, 100]
+    wl = resume_workload(shape, prefix, steps=2, seed=201, block_size=B)
     pre, last = split_last(wl)
-    say(f"[decode parity] {name}: prefixes {prefix}")
+    say(f"[decode parity] {name}: {len(prefix)} prefixes {prefix[:8]}, block size {B}")
     head = W.host_head_weights(shape, seed=42)
     if shape.hidden <= 512:
         host_w = W.host_weights(shape, seed=41, gain_std=0.1)
