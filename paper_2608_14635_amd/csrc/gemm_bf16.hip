@@ -439,12 +439,12 @@ __global__ __launch_bounds__(256) void splitk_epi_kernel(GemmParams p, int tiles
 // loads (per 128-k chunk a lane takes 64 contiguous bytes of its row) and
 // multiplies them with every row of A on v_mfma_f32_16x16x32_bf16 (16-row
 // tiles of A; rows past M are clamped and their results dropped).  No LDS
-// and no padding work: HBM-bound on the weights, while A stays in L2.  The
-// weight loads are plain (cached): a load instruction covers 64 bytes of
-// each of 16 rows, and the next one the rest of those lines, which
-// nontemporal loads would fetch again.  In a
-// chunk, MFMA t takes from lane group q = lane/16 the k values 32q+8t..+7 of
-// both operands, a fixed partition of the chunk's 128 k.  Output: the fp32
+// and no padding work: HBM-bound on the weights, while A stays in L2.  In a
+// chunk of 128 k, MFMA t takes the k values 32t+8q..+7 from lane group
+// q = lane/16 (the matrix core's own operand layout), so each load
+// instruction reads 64 contiguous bytes of each of 16 rows and the next one
+// the rest of those lines; the loads are plain (cached), as nontemporal ones
+// would fetch the lines again.  Output: the fp32
 // partial sums of the K range, in the split-K partial layout.
 constexpr int SK_CHUNK = 128;   // k per chunk
 constexpr int SK_UNROLL = 4;    // chunks in flight per wave
@@ -461,16 +461,18 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny_kernel(GemmParams p, int
   const int nb = item / p.ksplit, split = item % p.ksplit;
   const int tile_n = nb / (BN / 16), c0 = (nb % (BN / 16)) * 16;
   const int r16 = lane & 15, q = lane >> 4;
-  const bf16_t* brow = b_row_ptr(p, tile_n, c0 + r16) + 32 * q;
+  const bf16_t* brow = b_row_ptr(p, tile_n, c0 + r16) + 8 * q;
   const bf16_t* arow[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
-    arow[mt] = reinterpret_cast<const bf16_t*>(p.A) + (int64_t)min(mt * 16 + r16, p.M - 1) * p.lda + 32 * q;
+    arow[mt] = reinterpret_cast<const bf16_t*>(p.A) + (int64_t)min(mt * 16 + r16, p.M - 1) * p.lda + 8 * q;
   const int KC = p.K / SK_CHUNK;
   const int kc0 = split * kc_per, kc1 = min(KC, kc0 + kc_per);
   f32x4 acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  // SK_UNROLL chunks of loads in flight, then their MFMAs (the K range of a
+  // wave is a few chunks; a double-buffered loop measured slower here)
   for (int kc = kc0; kc < kc1; kc += SK_UNROLL) {
     bf16x8 bv[SK_UNROLL][4], av[SK_UNROLL][MT][4];
 #pragma unroll
@@ -478,12 +480,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny_kernel(GemmParams p, int
       if (kc + u < kc1) {
         const int ko = (kc + u) * SK_CHUNK;
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
-          bv[u][t] = *reinterpret_cast<const bf16x8*>(brow + ko + 8 * t);
+        for (int t = 0; t < 4; ++t) bv[u][t] = *reinterpret_cast<const bf16x8*>(brow + ko + 32 * t);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int t = 0; t < 4; ++t) av[u][mt][t] = *reinterpret_cast<const bf16x8*>(arow[mt] + ko + 8 * t);
+          for (int t = 0; t < 4; ++t) av[u][mt][t] = *reinterpret_cast<const bf16x8*>(arow[mt] + ko + 32 * t);
       }
     }
 #pragma unroll
