@@ -66,6 +66,10 @@ class Oracle:
             f.restype = C.c_int
             f.argtypes = [C.POINTER(_Model), C.c_void_p, C.POINTER(_Layer), I32P, I32P, C.c_int32,
                           I32P, C.c_int32, C.POINTER(_Arena), C.c_void_p]
+        self.lib.kvo_rebuild_from.restype = C.c_int
+        self.lib.kvo_rebuild_from.argtypes = [C.POINTER(_Model), C.c_void_p, C.POINTER(_Layer), I32P,
+                                              I32P, I32P, C.c_int32, I32P, C.c_int32,
+                                              C.POINTER(_Arena), C.c_void_p]
         self.lib.kvo_decode_step.restype = C.c_int
         self.lib.kvo_decode_step.argtypes = [C.POINTER(_Model), C.c_void_p, C.POINTER(_Layer), I32P,
                                              I32P, C.c_int32, I32P, C.c_int32, C.POINTER(_Arena),
@@ -141,6 +145,32 @@ class Oracle:
         rc = fn(C.byref(m), emb.ctypes.data, layers, tokens.ctypes.data_as(I32P),
                 lens.ctypes.data_as(I32P), len(lens), tables.ctypes.data_as(I32P), max_blocks,
                 C.byref(ar), fh.ctypes.data if fh is not None else None)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        return fh
+
+    def rebuild_from(self, shape, weights: Dict, tokens, lens, starts, tables, arena: np.ndarray,
+                     block_size: int, num_blocks: int, dtype: Optional[int] = None,
+                     final_hidden: bool = False):
+        """Recompute positions starts[r] .. lens[r]-1 in place on `arena`, the
+        prefixes' K/V being read from it; tokens holds the recomputed
+        positions' tokens only (kvo.h defines it)."""
+        dt = shape.dtype if dtype is None else dtype
+        m = self._model(shape, dt)
+        tokens, lens, starts = self._i32(tokens), self._i32(lens), self._i32(starts)
+        tables = self._i32(tables)
+        max_blocks = tables.shape[1] if tables.ndim == 2 else 0
+        layers = self._layers(weights, dt)
+        emb = self._check(weights["embed"], dt)
+        ar = self._arena(shape, arena, block_size, num_blocks, dt)
+        assert tokens.shape[0] == int((lens - starts).sum()) and len(starts) == len(lens)
+        nrows = int((lens - starts).sum())
+        fh = np.zeros((nrows, shape.hidden), np.float64) if final_hidden else None
+        I32P = C.POINTER(C.c_int32)
+        rc = self.lib.kvo_rebuild_from(C.byref(m), emb.ctypes.data, layers, tokens.ctypes.data_as(I32P),
+                                       lens.ctypes.data_as(I32P), starts.ctypes.data_as(I32P), len(lens),
+                                       tables.ctypes.data_as(I32P), max_blocks, C.byref(ar),
+                                       fh.ctypes.data if fh is not None else None)
         if rc != 0:
             raise ValueError("oracle rejected its arguments")
         return fh

@@ -316,6 +316,49 @@ static void embed_rows(const kvo_model* m, const void* embed, const int32_t* tok
     for (j = 0; j < H; ++j) x[r * H + j] = to_work(load(embed, m->dtype, (int64_t)tok[r] * H + j), m->dtype);
 }
 
+int kvo_rebuild_from(const kvo_model* m, const void* embed, const kvo_layer* layers,
+                     const int32_t* tokens, const int32_t* lens, const int32_t* starts,
+                     int32_t num_requests, const int32_t* block_tables, int32_t max_blocks,
+                     kvo_arena* arena, double* final_hidden) {
+  int64_t off = 0;
+  int32_t r;
+  if (!m || !lens || !starts || num_requests < 0 || !arena || !arena->base || arena->block_size <= 0)
+    return -1;
+  if (m->num_q_heads % m->num_kv_heads != 0 || m->head_dim % 2 != 0) return -1;
+  for (r = 0; r < num_requests; ++r) {
+    const int64_t n = lens[r], s = starts[r];
+    int64_t p, b;
+    if (n < 0 || s < 0 || s > n || (n + arena->block_size - 1) / arena->block_size > max_blocks) return -1;
+    for (p = 0; p < n - s; ++p)
+      if (tokens[off + p] < 0 || tokens[off + p] >= m->vocab) return -1;
+    for (b = 0; b < (n + arena->block_size - 1) / arena->block_size; ++b) {
+      const int32_t blk = block_tables[(int64_t)r * max_blocks + b];
+      if (blk < 0 || blk >= arena->num_blocks) return -1;
+    }
+    off += n - s;
+  }
+  off = 0;
+  for (r = 0; r < num_requests; ++r) {
+    const int64_t s = starts[r], cnt = lens[r] - starts[r], H = m->hidden;
+    const int32_t* table = block_tables + (int64_t)r * max_blocks;
+    double *x, *scratch;
+    int l;
+    if (cnt == 0) continue;
+    x = (double*)malloc(sizeof(double) * (size_t)(cnt * H));
+    scratch = (double*)malloc(sizeof(double) * scratch_elems(m, cnt));
+    embed_rows(m, embed, tokens + off, cnt, x);
+    for (l = 0; l < m->num_layers; ++l) {
+      const int kv_only = (l == m->num_layers - 1) && final_hidden == NULL;
+      layer_step(m, &layers[l], l, x, s, cnt, table, arena, kv_only, scratch);
+    }
+    if (final_hidden) memcpy(final_hidden + off * H, x, sizeof(double) * (size_t)(cnt * H));
+    free(scratch);
+    free(x);
+    off += cnt;
+  }
+  return 0;
+}
+
 int kvo_rebuild(const kvo_model* m, const void* embed, const kvo_layer* layers,
                 const int32_t* tokens, const int32_t* lens, int32_t num_requests,
                 const int32_t* block_tables, int32_t max_blocks, kvo_arena* arena,

@@ -106,6 +106,22 @@ int kvo_layer0_kv(const kvo_model* m, const void* embed, const kvo_layer* layer0
 int kvo_time_layers(const kvo_model* m, const void* embed, const kvo_layer* layers,
                     const int32_t* tokens, int32_t n, int32_t num_layers);
 
+/* Rebuild from a retained prefix (partial recovery and shared-prefix reuse,
+ * the two ways of not recomputing K/V the pool still holds): request r's
+ * positions starts[r] .. lens[r]-1 are recomputed and written, while the K/V of
+ * positions 0 .. starts[r]-1 are taken as already in the arena (its table
+ * entries for them are read, their slots are not written).  tokens packs the
+ * recomputed positions' tokens only: sum of (lens[r] - starts[r]).  Attention
+ * of every recomputed position covers positions 0 .. p, reading the prefix
+ * K/V from the arena.  With all starts 0 this is kvo_rebuild.  final_hidden
+ * (optional) has one row per recomputed position.  Returns 0, or -1 on an
+ * invalid argument (a start outside [0, len], a token or table entry out of
+ * range). */
+int kvo_rebuild_from(const kvo_model* m, const void* embed, const kvo_layer* layers,
+                     const int32_t* tokens, const int32_t* lens, const int32_t* starts,
+                     int32_t num_requests, const int32_t* block_tables, int32_t max_blocks,
+                     kvo_arena* arena, double* final_hidden);
+
 /* Commit digest of one block (flush-free recovery; the paper flushes the
  * whole pool because it cannot tell which KV contents survived intact, and
  * leaves fine-grained consistency tracking to future work: Sec. 4.2 flush

@@ -17,6 +17,9 @@ What pins what:
     GQA == MHA with duplicated KV heads; causality; batch independence;
     idempotence over garbage; exact placement and untouched bits
   * library routine: fp32 -> bf16 rounding against torch's conversion
+  * rebuild from a retained prefix: two-phase rebuild == full rebuild
+    (causality), start 0 == rebuild, start = length is a no-op, the suffix
+    reads the prefix K/V the arena holds, shared-prefix block copies
   * block commit digests: closed forms on arenas built to cancel the word
     keys (N c^2, one changed word), bit flips always detected, bytes outside
     the covered slots ignored, leading-intact counts with planted corruption
@@ -598,6 +601,109 @@ def pin_resume_from_rebuild_equals_decode_built(o):
         t_de, z_de, a_de = _resume(o, shape, w, head, wl, "decode", 5)
         assert np.array_equal(t_re, t_de) and np.array_equal(z_re, z_de)
         assert np.array_equal(a_re, a_de)
+
+
+# --------------------------------------------------------------------------
+# rebuild from a retained prefix
+# --------------------------------------------------------------------------
+def _piece(wl, lo, hi):
+    """Packed tokens of positions lo[r] .. hi[r]-1 of every request."""
+    offs = wl.request_offsets()
+    parts = [wl.tokens[offs[r] + int(lo[r]):offs[r] + int(hi[r])] for r in range(wl.num_requests)]
+    return np.concatenate(parts).astype(np.int32) if parts else np.zeros(0, np.int32)
+
+
+def pin_rebuild_from_split_equals_full(o):
+    """A position's K/V depend only on the tokens up to it (causality):
+    rebuilding positions [0, s) and then [s, n) from the retained prefix gives
+    the full rebuild's arena bit for bit, with s at 0, at n, at and inside
+    block boundaries, for fp32 and bf16 models."""
+    for shape, seed in ((TINY_GQA, 51), (TINY_BF16_2L, 52)):
+        w = W.host_weights(shape, seed=seed)
+        wl = W.small_workload(shape, [1, 17, 40, 33, 0, 9], block_size=8, seed=150 + seed,
+                              other_live_frac=0.25)
+        B, NB = wl.block_size, wl.num_blocks
+        full = W.host_arena(wl)
+        o.rebuild(shape, w, wl.tokens, wl.lens, wl.block_tables, full, B, NB)
+        starts = np.array([0, 16, 23, 33, 0, 9], np.int32)
+        two = W.host_arena(wl)
+        zero = np.zeros_like(starts)
+        o.rebuild(shape, w, _piece(wl, zero, starts), starts, wl.block_tables, two, B, NB)
+        o.rebuild_from(shape, w, _piece(wl, starts, wl.lens), wl.lens, starts, wl.block_tables, two, B, NB)
+        assert np.array_equal(two, full), shape
+
+
+def pin_rebuild_from_boundaries(o):
+    """Start 0 is the plain rebuild (bit for bit); start = length changes
+    nothing at all."""
+    shape = TINY_GQA
+    w = W.host_weights(shape, seed=53)
+    wl = W.small_workload(shape, [5, 16, 29], seed=153, other_live_frac=0.25)
+    B, NB = wl.block_size, wl.num_blocks
+    a = W.host_arena(wl)
+    o.rebuild(shape, w, wl.tokens, wl.lens, wl.block_tables, a, B, NB)
+    b = W.host_arena(wl)
+    zero = np.zeros(wl.num_requests, np.int32)
+    o.rebuild_from(shape, w, wl.tokens, wl.lens, zero, wl.block_tables, b, B, NB)
+    assert np.array_equal(a, b)
+    c = a.copy()
+    o.rebuild_from(shape, w, np.zeros(0, np.int32), wl.lens, wl.lens, wl.block_tables, c, B, NB)
+    assert np.array_equal(a, c)
+
+
+def pin_rebuild_from_reads_retained_prefix(o):
+    """The recomputed positions attend to the prefix K/V the arena holds: with
+    one request's prefix slots holding another model's K/V, its recomputed
+    layer-0 K/V (which precede any attention) are unchanged, its later
+    layers' change, and the other requests are untouched."""
+    shape = TINY_GQA
+    w, w2 = W.host_weights(shape, seed=54), W.host_weights(shape, seed=55)
+    wl = W.small_workload(shape, [24, 24], block_size=8, seed=154, other_live_frac=0.0)
+    B, NB = wl.block_size, wl.num_blocks
+    starts = np.array([16, 16], np.int32)
+    good, bad = W.host_arena(wl), W.host_arena(wl)
+    o.rebuild(shape, w, wl.tokens, wl.lens, wl.block_tables, good, B, NB)
+    o.rebuild(shape, w2, wl.tokens, wl.lens, wl.block_tables, bad, B, NB)
+    mixed = good.copy()
+    view_m = mixed.reshape(shape.num_layers, 2, NB, B, -1)
+    view_b = bad.reshape(shape.num_layers, 2, NB, B, -1)
+    for j in range(2):  # request 1's two prefix blocks from the other model
+        view_m[:, :, wl.block_tables[1, j]] = view_b[:, :, wl.block_tables[1, j]]
+    o.rebuild_from(shape, w, _piece(wl, starts, wl.lens), wl.lens, starts, wl.block_tables, mixed, B, NB)
+    vg = good.reshape(shape.num_layers, 2, NB, B, -1)
+    blk0, blk1 = wl.block_tables[0, 2], wl.block_tables[1, 2]   # the recomputed block
+    assert np.array_equal(view_m[:, :, blk0], vg[:, :, blk0])
+    assert np.array_equal(view_m[0, :, blk1], vg[0, :, blk1])
+    assert not np.array_equal(view_m[1:, :, blk1], vg[1:, :, blk1])
+
+
+def pin_shared_prefix_block_copy(o):
+    """Shared-prefix reuse: requests beginning with the same S tokens (S a
+    multiple of the block size); the first is rebuilt in full, its first S/B
+    blocks are copied into the others' first blocks, and the others are
+    rebuilt from S: the arena equals the full rebuild of every request."""
+    shape = TINY_BF16_2L
+    w = W.host_weights(shape, seed=56)
+    wl = W.small_workload(shape, [40, 21, 16, 57], block_size=8, seed=156, other_live_frac=0.25)
+    B, NB, S = wl.block_size, wl.num_blocks, 16
+    offs = wl.request_offsets()
+    toks = wl.tokens.copy()
+    for r in range(1, wl.num_requests):
+        toks[offs[r]:offs[r] + S] = toks[:S]
+    wl = dataclasses.replace(wl, tokens=toks)
+    full = W.host_arena(wl)
+    o.rebuild(shape, w, wl.tokens, wl.lens, wl.block_tables, full, B, NB)
+    arena = W.host_arena(wl)
+    first = dataclasses.replace(wl, lens=wl.lens[:1], tokens=wl.tokens[:wl.lens[0]],
+                                block_tables=wl.block_tables[:1])
+    o.rebuild(shape, w, first.tokens, first.lens, first.block_tables, arena, B, NB)
+    view = arena.reshape(shape.num_layers, 2, NB, B, -1)
+    for r in range(1, wl.num_requests):
+        for j in range(S // B):
+            view[:, :, wl.block_tables[r, j]] = view[:, :, wl.block_tables[0, j]]
+    starts = np.array([wl.lens[0]] + [S] * (wl.num_requests - 1), np.int32)
+    o.rebuild_from(shape, w, _piece(wl, starts, wl.lens), wl.lens, starts, wl.block_tables, arena, B, NB)
+    assert np.array_equal(arena, full)
 
 
 # --------------------------------------------------------------------------

@@ -52,6 +52,10 @@ MUTANTS = [
      "to_work(dot_row(W, dt, i, K, A + r * K), dt)", 0),
     ("v_bias_from_k", "project_bias(lw->wv, lw->bv, dt, nkv * d, H, a, cnt, v);",
      "project_bias(lw->wv, lw->bk, dt, nkv * d, H, a, cnt, v);", 0),
+    ("rebuild_from_positions_from_zero", "layer_step(m, &layers[l], l, x, s, cnt, table, arena, kv_only, scratch);",
+     "layer_step(m, &layers[l], l, x, 0, cnt, table, arena, kv_only, scratch);", 0),
+    ("rebuild_from_token_offset", "    off += cnt;", "    off += lens[r];", 0),
+    ("rebuild_from_first_tokens", "embed_rows(m, embed, tokens + off, cnt, x);", "embed_rows(m, embed, tokens, cnt, x);", 0),
     ("digest_key_multiplier", "u ^ (uint32_t)(i * 0x9E3779B9u)", "u ^ (uint32_t)(i * 0x9E3779B1u)", 0),
     ("digest_unkeyed", "u ^ (uint32_t)(i * 0x9E3779B9u)", "u", 0),
     ("digest_key_restarts_per_plane", "for (s = 0; s < nslots; ++s) {", "for (s = 0, i = 0; s < nslots; ++s) {", 0),
