@@ -17,6 +17,7 @@
 #include "kvr.h"
 #include "kvr_decode.h"
 #include "kvr_verify.h"
+#include "kvr_reuse.h"
 #include "kvr_profile.h"
 #include "launch.h"
 
@@ -106,18 +107,27 @@ bool same_desc(const kv_model_desc& a, const kv_model_desc& b) {
 // host->device copy stages it)
 // ---------------------------------------------------------------------------
 struct Layout {
-  int64_t T = 0, W = 0, Wpad = 0, nqblk_cap = 0;
-  size_t tok = 0, pos = 0, slot = 0, qblk = 0, meta_end = 0;
+  int64_t Tg = 0, W = 0, Wpad = 0, Tk = 0, Wk = 0, Wkpad = 0, nqblk_cap = 0, nseg_cap = 0;
+  size_t tok = 0, pos = 0, slot = 0, krow = 0, kslot = 0, qblk = 0, seg = 0, meta_end = 0;
   size_t rope = 0, x = 0, a = 0, q = 0, u = 0, vt = 0, kc = 0, hf = 0, total = 0;
 };
 
-// T and W count wave rows: each request occupies round_up(len, ROW_ALIGN) rows.
-Layout make_layout(const kv_model_desc& d, int32_t R, int64_t T, int64_t W) {
+// Two row spaces.  Rows (Tg in all, W per wave) are the positions computed:
+// each request occupies round_up(len - start, ROW_ALIGN) of them.  Key rows
+// (Tk, Wk) hold the K/V copies attention reads: round_up(start + its rows,
+// ROW_ALIGN) per request, the retained prefix first.  With every start 0 the
+// two spaces coincide.  nseg_cap bounds the prefix-gather segments.
+Layout make_layout(const kv_model_desc& d, int32_t R, int64_t Tg, int64_t W, int64_t Tk, int64_t Wk,
+                   int64_t nseg_cap) {
   Layout L;
-  L.T = T;
+  L.Tg = Tg;
   L.W = W;
   L.Wpad = round_up(std::max<int64_t>(W, 1), 256);
-  L.nqblk_cap = (T + ATTN_QBLOCK_MIN - 1) / ATTN_QBLOCK_MIN + R;
+  L.Tk = Tk;
+  L.Wk = Wk;
+  L.Wkpad = round_up(std::max<int64_t>(Wk, 1), 256);
+  L.nqblk_cap = (Tg + ATTN_QBLOCK_MIN - 1) / ATTN_QBLOCK_MIN + R;
+  L.nseg_cap = nseg_cap;
   const int64_t e = elem_bytes(d.dtype);
   size_t off = 0;
   auto seg = [&](size_t bytes) {
@@ -125,18 +135,21 @@ Layout make_layout(const kv_model_desc& d, int32_t R, int64_t T, int64_t W) {
     off = (size_t)round_up((int64_t)(off + bytes), 256);
     return at;
   };
-  L.tok = seg(4 * (size_t)T);
-  L.pos = seg(4 * (size_t)T);
-  L.slot = seg(8 * (size_t)T);
+  L.tok = seg(4 * (size_t)Tg);
+  L.pos = seg(4 * (size_t)Tg);
+  L.slot = seg(8 * (size_t)Tg);
+  L.krow = seg(4 * (size_t)Tg);
+  L.kslot = seg(8 * (size_t)Tk);
   L.qblk = seg(16 * (size_t)L.nqblk_cap);
+  L.seg = seg(8 * (size_t)nseg_cap);
   L.meta_end = off;
-  L.rope = seg((size_t)8 * L.Wpad * (d.head_dim / 2));
+  L.rope = seg((size_t)8 * L.Wkpad * (d.head_dim / 2));
   L.x = seg((size_t)4 * L.Wpad * d.hidden);
   L.a = seg((size_t)e * L.Wpad * d.hidden);
   L.q = seg((size_t)e * L.Wpad * d.num_q_heads * d.head_dim);
   L.u = seg((size_t)e * L.Wpad * d.num_q_heads * d.head_dim);
-  L.vt = seg(d.dtype == KV_BF16 ? (size_t)2 * d.num_kv_heads * d.head_dim * L.Wpad : 0);
-  L.kc = seg(d.dtype == KV_BF16 ? (size_t)2 * d.num_kv_heads * d.head_dim * L.Wpad : 0);
+  L.vt = seg(d.dtype == KV_BF16 ? (size_t)2 * d.num_kv_heads * d.head_dim * L.Wkpad : 0);
+  L.kc = seg(d.dtype == KV_BF16 ? (size_t)2 * d.num_kv_heads * d.head_dim * L.Wkpad : 0);
   L.hf = seg((size_t)e * L.Wpad * d.ffn_dim);
   L.total = off;
   return L;
@@ -147,12 +160,23 @@ Layout make_layout(const kv_model_desc& d, int32_t R, int64_t T, int64_t W) {
 // ---------------------------------------------------------------------------
 int64_t padded_rows(int64_t n) { return n > 0 ? round_up(n, ROW_ALIGN) : 0; }
 
+// Key rows a wave gets for a row capacity W: the rows' share of all key
+// rows, at least the largest request's key rows.
+int64_t key_capacity(int64_t W, int64_t Tg, int64_t Tk, int64_t kmax) {
+  if (Tg <= 0) return kmax;
+  const int64_t prop = round_up((W * Tk + Tg - 1) / Tg, ROW_ALIGN);
+  return std::max(kmax, std::min(Tk, prop));
+}
+
 struct Wave {
-  int64_t tok_begin;  // first metadata row of the wave
+  int64_t tok_begin;  // first row of the wave
   int32_t rows;       // rows including per-request padding (a multiple of ROW_ALIGN)
+  int64_t key_begin;  // first key row of the wave
+  int32_t keys;       // key rows
   int32_t qblk_begin, num_qblk;
-  double causal_pairs;  // sum over its requests of n(n+1)/2 (query, key) pairs
-  int64_t tokens;       // real (unpadded) tokens
+  int32_t seg_begin, num_seg;
+  double causal_pairs;  // (query, key) pairs of its computed positions
+  int64_t tokens;       // real (unpadded) computed positions
 };
 
 }  // namespace
@@ -186,7 +210,8 @@ struct kv_plan {
   uint64_t ws_bytes;
   Layout lay;
   std::vector<Wave> waves;
-  int32_t max_len;
+  int32_t max_len;   // longest request with positions to compute
+  bool has_prefix;   // some request starts past position 0
 };
 
 namespace {
@@ -219,9 +244,15 @@ struct DeviceGuard {
   }
 };
 
+// starts may be null (every request from position 0).  Rules for starts:
+// 0 <= start <= len, start a multiple of 8 unless equal to len.  Blocks:
+// a block holding a position >= start of its request is written and may be
+// listed by no other request for writing, nor read as prefix by an earlier
+// request; a block holding only positions < start is read and may be shared,
+// also with an earlier request that writes it.
 kv_status check_request(const kv_model_desc* desc, int32_t B, int64_t NB, const int32_t* tokens,
                         const int32_t* lens, int32_t R, const int32_t* tables, int32_t max_blocks,
-                        int64_t* total_out, int32_t* max_len_out) {
+                        int64_t* total_out, int32_t* max_len_out, const int32_t* starts = nullptr) {
   kv_status st = check_desc(desc);
   if (st != KV_OK) return st;
   if (B <= 0 || NB <= 0) return fail(KV_EINVAL, "block_size and num_blocks must be positive");
@@ -232,12 +263,17 @@ kv_status check_request(const kv_model_desc* desc, int32_t B, int64_t NB, const 
   int32_t max_len = 0;
   for (int32_t r = 0; r < R; ++r) {
     if (lens[r] < 0) return fail(KV_EINVAL, "prefix_lens[%d] = %d < 0", r, lens[r]);
-    T += lens[r];
+    const int32_t s0 = starts ? starts[r] : 0;
+    if (s0 < 0 || s0 > lens[r])
+      return fail(KV_EINVAL, "starts[%d] = %d outside [0, %d]", r, s0, lens[r]);
+    if (s0 % 8 != 0 && s0 != lens[r])
+      return fail(KV_EINVAL, "starts[%d] = %d is not a multiple of 8", r, s0);
+    T += lens[r] - s0;
     max_len = std::max(max_len, lens[r]);
   }
   if (T > (int64_t)INT32_MAX) return fail(KV_EINVAL, "more than 2^31-1 prefix tokens in one call");
   if (T > 0 && !tokens) return fail(KV_EINVAL, "null token_prefixes");
-  if (T > 0 && !tables) return fail(KV_EINVAL, "null block_tables");
+  if ((T > 0 || (starts && max_len > 0)) && !tables) return fail(KV_EINVAL, "null block_tables");
   for (int32_t r = 0; r < R; ++r) {
     const int64_t nb = ((int64_t)lens[r] + B - 1) / B;
     if (nb > max_blocks)
@@ -248,18 +284,32 @@ kv_status check_request(const kv_model_desc* desc, int32_t B, int64_t NB, const 
     if (tokens[i] < 0 || tokens[i] >= desc->vocab)
       return fail(KV_ERANGE, "token %d at index %lld outside [0, %d)", tokens[i], (long long)i,
                   desc->vocab);
-  std::vector<uint8_t> seen((size_t)NB, 0);
+  // writer of each block (-1: none)
+  std::vector<int32_t> writer((size_t)NB, -1);
   for (int32_t r = 0; r < R; ++r) {
     const int64_t nb = ((int64_t)lens[r] + B - 1) / B;
+    const int64_t s0 = starts ? starts[r] : 0;
     for (int64_t b = 0; b < nb; ++b) {
       const int32_t blk = tables[(int64_t)r * max_blocks + b];
       if (blk < 0 || blk >= NB)
         return fail(KV_ERANGE, "block_tables[%d][%lld] = %d outside [0, %lld)", r, (long long)b,
                     blk, (long long)NB);
-      if (seen[blk]) return fail(KV_EALIAS, "block %d listed twice", blk);
-      seen[blk] = 1;
+      if ((b + 1) * B > s0 && s0 < lens[r]) {  // holds a position >= start: written
+        if (writer[blk] >= 0) return fail(KV_EALIAS, "block %d listed twice", blk);
+        writer[blk] = r;
+      }
     }
   }
+  if (starts)
+    for (int32_t r = 0; r < R; ++r) {
+      const int64_t s0 = starts[r];
+      for (int64_t b = 0; b * B < s0; ++b) {  // holds a position < start: read
+        const int32_t blk = tables[(int64_t)r * max_blocks + b];
+        if (writer[blk] > r)
+          return fail(KV_EALIAS, "block %d is read by request %d before request %d writes it", blk, r,
+                      writer[blk]);
+      }
+    }
   if (total_out) *total_out = T;
   if (max_len_out) *max_len_out = max_len;
   return KV_OK;
@@ -404,8 +454,20 @@ uint64_t kv_rebuild_workspace_bytes(const kv_model_desc* desc, int32_t num_reque
     return 0;
   // every request may add up to ROW_ALIGN - 1 padding rows
   const int64_t pad = (int64_t)(ROW_ALIGN - 1) * num_requests;
-  return make_layout(*desc, num_requests, total_tokens + pad,
-                     std::min(wave_tokens, total_tokens) + pad).total;
+  const int64_t W = std::min(wave_tokens, total_tokens) + pad;
+  return make_layout(*desc, num_requests, total_tokens + pad, W, total_tokens + pad, W, 0).total;
+}
+
+uint64_t kv_rebuild_from_workspace_bytes(const kv_model_desc* desc, int32_t num_requests,
+                                         int64_t total_rows, int64_t total_keys, int64_t wave_rows) {
+  if (check_desc(desc) != KV_OK || num_requests < 0 || total_rows < 0 || total_keys < total_rows ||
+      wave_rows < 0)
+    return 0;
+  const int64_t pad = (int64_t)(ROW_ALIGN - 1) * num_requests;
+  const int64_t Tg = total_rows + pad, Tk = total_keys + 2 * pad;
+  const int64_t W = std::min(wave_rows, total_rows) + pad;
+  const int64_t nseg = (total_keys - total_rows) / GATHER_KEYS + num_requests + 1;
+  return make_layout(*desc, num_requests, Tg, W, Tk, key_capacity(W, Tg, Tk, 0), nseg).total;
 }
 
 kv_status kv_rebuild_check(const kv_model_desc* desc, int32_t block_size, int64_t num_blocks,
@@ -503,16 +565,18 @@ kv_status kv_arena_release(kv_arena_t a) {
   return ok();
 }
 
-kv_status kv_rebuild_stage(kv_arena_t arena, const int32_t* tokens, const int32_t* lens, int32_t R,
-                           const int32_t* tables, int32_t max_blocks, void* workspace,
-                           uint64_t ws_bytes, void* stream, kv_plan_t* out) {
+namespace {
+
+kv_status stage_impl(kv_arena_t arena, const int32_t* tokens, const int32_t* lens,
+                     const int32_t* starts, int32_t R, const int32_t* tables, int32_t max_blocks,
+                     void* workspace, uint64_t ws_bytes, void* stream, kv_plan_t* out) {
   if (!out) return fail(KV_EINVAL, "null output plan");
   *out = nullptr;
   if (!live_arena(arena)) return fail(KV_ESTATE, "unknown or released arena handle");
   int64_t T = 0;
   int32_t max_len = 0;
   kv_status st = check_request(&arena->desc, arena->block_size, arena->num_blocks, tokens, lens, R,
-                               tables, max_blocks, &T, &max_len);
+                               tables, max_blocks, &T, &max_len, starts);
   if (st != KV_OK) return st;
   const kv_model_desc& d = arena->desc;
   kv_plan* plan = new (std::nothrow) kv_plan();
@@ -521,49 +585,78 @@ kv_status kv_rebuild_stage(kv_arena_t arena, const int32_t* tokens, const int32_
   plan->ws = reinterpret_cast<char*>(workspace);
   plan->ws_bytes = ws_bytes;
   plan->max_len = max_len;
+  plan->has_prefix = false;
   if (T > 0) {
     if (!workspace) {
       delete plan;
       return fail(KV_EINVAL, "null workspace");
     }
-    // wave rows: each request starts on a ROW_ALIGN boundary; its padding rows
-    // carry token 0, position 0 and slot -1 (computed, never scattered)
-    std::vector<int64_t> req_off(R + 1, 0), row_off(R + 1, 0);
+    // rows: each request's computed positions start on a ROW_ALIGN boundary;
+    // padding rows carry token 0, position 0 and slot -1 (computed, never
+    // scattered).  Key rows: the retained prefix, then the computed rows.
+    std::vector<int32_t> st0(R, 0);
+    for (int32_t r = 0; r < R; ++r) st0[r] = starts ? starts[r] : 0;
+    std::vector<int64_t> tok_off(R + 1, 0), row_off(R + 1, 0), key_off(R + 1, 0);
+    int64_t gmax = 0, kmax = 0, nseg = 0;
     for (int32_t r = 0; r < R; ++r) {
-      req_off[r + 1] = req_off[r] + lens[r];
-      row_off[r + 1] = row_off[r] + padded_rows(lens[r]);
+      const int64_t n = lens[r] - st0[r];
+      const int64_t g = padded_rows(n);
+      const int64_t k = n > 0 ? round_up(st0[r] + g, ROW_ALIGN) : 0;
+      tok_off[r + 1] = tok_off[r] + n;
+      row_off[r + 1] = row_off[r] + g;
+      key_off[r + 1] = key_off[r] + k;
+      gmax = std::max(gmax, g);
+      kmax = std::max(kmax, k);
+      if (n > 0 && st0[r] > 0) {
+        nseg += (st0[r] + GATHER_KEYS - 1) / GATHER_KEYS;
+        plan->has_prefix = true;
+      }
     }
-    const int64_t Trows = row_off[R];
-    const int64_t min_wave = padded_rows(max_len);
-    const Layout smallest = make_layout(d, R, Trows, min_wave);
+    int32_t max_active = 0;
+    for (int32_t r = 0; r < R; ++r)
+      if (lens[r] > st0[r]) max_active = std::max(max_active, lens[r]);
+    plan->max_len = max_active;
+    const int64_t Tg = row_off[R], Tk = key_off[R];
+    const Layout smallest = make_layout(d, R, Tg, gmax, Tk, kmax, nseg);
     if (smallest.total > ws_bytes) {
       delete plan;
       return fail(KV_ENOMEM, "workspace of %llu bytes < %llu needed for the longest request",
                   (unsigned long long)ws_bytes, (unsigned long long)smallest.total);
     }
-    // largest wave capacity whose layout fits
-    int64_t lo = min_wave, hi = Trows;
+    // largest row capacity whose layout fits
+    int64_t lo = gmax, hi = Tg;
     while (lo < hi) {
       const int64_t mid = lo + (hi - lo + 1) / 2;
-      if (make_layout(d, R, Trows, mid).total <= ws_bytes) lo = mid; else hi = mid - 1;
+      if (make_layout(d, R, Tg, mid, Tk, key_capacity(mid, Tg, Tk, kmax), nseg).total <= ws_bytes)
+        lo = mid;
+      else
+        hi = mid - 1;
     }
-    plan->lay = make_layout(d, R, Trows, lo);
+    plan->lay = make_layout(d, R, Tg, lo, Tk, key_capacity(lo, Tg, Tk, kmax), nseg);
     const Layout& L = plan->lay;
 
-    // waves: consecutive requests, never split
+    // waves: consecutive requests, never split, within both capacities
+    std::vector<int32_t> wave_of(R, -1);
     {
-      Wave w{0, 0, 0, 0, 0.0, 0};
+      Wave w{0, 0, 0, 0, 0, 0, 0, 0, 0.0, 0};
       for (int32_t r = 0; r < R; ++r) {
-        if (lens[r] == 0) continue;
-        const int64_t pr = padded_rows(lens[r]);
-        if (w.rows > 0 && w.rows + pr > L.W) {
+        const int64_t n = lens[r] - st0[r];
+        if (n == 0) continue;
+        const int64_t g = row_off[r + 1] - row_off[r], k = key_off[r + 1] - key_off[r];
+        if (w.rows > 0 && (w.rows + g > L.W || w.keys + k > L.Wk)) {
           plan->waves.push_back(w);
-          w = Wave{row_off[r], 0, 0, 0, 0.0, 0};
+          w = Wave{row_off[r], 0, key_off[r], 0, 0, 0, 0, 0, 0.0, 0};
         }
-        if (w.rows == 0) w.tok_begin = row_off[r];
-        w.rows += (int32_t)pr;
-        w.causal_pairs += 0.5 * (double)lens[r] * ((double)lens[r] + 1.0);
-        w.tokens += lens[r];
+        if (w.rows == 0) {
+          w.tok_begin = row_off[r];
+          w.key_begin = key_off[r];
+        }
+        w.rows += (int32_t)g;
+        w.keys += (int32_t)k;
+        const double a = (double)st0[r], b = (double)lens[r];
+        w.causal_pairs += 0.5 * (b * (b + 1.0) - a * (a + 1.0));
+        w.tokens += n;
+        wave_of[r] = (int32_t)plan->waves.size();
       }
       if (w.rows > 0) plan->waves.push_back(w);
     }
@@ -589,39 +682,56 @@ kv_status kv_rebuild_stage(kv_arena_t arena, const int32_t* tokens, const int32_
     int32_t* htok = reinterpret_cast<int32_t*>(hb + L.tok);
     int32_t* hpos = reinterpret_cast<int32_t*>(hb + L.pos);
     int64_t* hslot = reinterpret_cast<int64_t*>(hb + L.slot);
+    int32_t* hkrow = reinterpret_cast<int32_t*>(hb + L.krow);
+    int64_t* hkslot = reinterpret_cast<int64_t*>(hb + L.kslot);
     int4* hq = reinterpret_cast<int4*>(hb + L.qblk);
+    int2* hseg = reinterpret_cast<int2*>(hb + L.seg);
     const int32_t B = arena->block_size;
     for (int32_t r = 0; r < R; ++r) {
+      const int32_t n = lens[r] - st0[r];
+      if (n == 0) continue;
+      const Wave& w = plan->waves[wave_of[r]];
       const int32_t* tab = tables + (int64_t)r * max_blocks;
-      const int64_t r0 = row_off[r];
-      for (int32_t p = 0; p < lens[r]; ++p) {
-        htok[r0 + p] = tokens[req_off[r] + p];
-        hpos[r0 + p] = p;
-        hslot[r0 + p] = (int64_t)tab[p / B] * B + p % B;
+      const int64_t r0 = row_off[r], k0 = key_off[r];
+      const int32_t kloc = (int32_t)(k0 - w.key_begin) + st0[r];  // key row of the first computed position
+      for (int32_t i = 0; i < n; ++i) {
+        const int32_t p = st0[r] + i;
+        htok[r0 + i] = tokens[tok_off[r] + i];
+        hpos[r0 + i] = p;
+        hslot[r0 + i] = (int64_t)tab[p / B] * B + p % B;
+        hkrow[r0 + i] = kloc + i;
       }
-      for (int64_t t = r0 + lens[r]; t < row_off[r + 1]; ++t) {
+      for (int64_t t = r0 + n; t < row_off[r + 1]; ++t) {
         htok[t] = 0;
         hpos[t] = 0;
         hslot[t] = -1;
+        hkrow[t] = kloc + (int32_t)(t - r0);
       }
+      for (int32_t p = 0; p < lens[r]; ++p) hkslot[k0 + p] = (int64_t)tab[p / B] * B + p % B;
+      for (int64_t t = k0 + lens[r]; t < key_off[r + 1]; ++t) hkslot[t] = -1;
     }
     const int QB = attn_qblock(d.dtype, d.num_q_heads / d.num_kv_heads);
-    int32_t nq_total = 0;
-    for (auto& w : plan->waves) {
+    int32_t nq_total = 0, ns_total = 0;
+    for (size_t wi = 0; wi < plan->waves.size(); ++wi) {
+      Wave& w = plan->waves[wi];
       w.qblk_begin = nq_total;
+      w.seg_begin = ns_total;
       std::vector<int4> blocks;
       for (int32_t r = 0; r < R; ++r) {
-        if (lens[r] == 0 || row_off[r] < w.tok_begin || row_off[r] >= w.tok_begin + w.rows) continue;
-        const int32_t rs = (int32_t)(row_off[r] - w.tok_begin);
-        for (int32_t qs = 0; qs < lens[r]; qs += QB)
-          blocks.push_back(make_int4(rs + qs, std::min(QB, lens[r] - qs), rs, 0));
+        if (wave_of[r] != (int32_t)wi) continue;
+        const int32_t n = lens[r] - st0[r];
+        const int32_t rs = (int32_t)(row_off[r] - w.tok_begin), ks = (int32_t)(key_off[r] - w.key_begin);
+        for (int32_t qs = 0; qs < n; qs += QB)
+          blocks.push_back(make_int4(rs + qs, std::min(QB, n - qs), ks, st0[r] + qs));
+        for (int32_t p0 = 0; p0 < st0[r]; p0 += GATHER_KEYS)
+          hseg[ns_total++] = make_int2(ks + p0, std::min(GATHER_KEYS, st0[r] - p0));
       }
       // longest causal extent first
-      std::stable_sort(blocks.begin(), blocks.end(), [](const int4& x, const int4& y) {
-        return (x.x + x.y - x.z) > (y.x + y.y - y.z);
-      });
+      std::stable_sort(blocks.begin(), blocks.end(),
+                       [](const int4& x, const int4& y) { return (x.w + x.y) > (y.w + y.y); });
       std::memcpy(hq + nq_total, blocks.data(), sizeof(int4) * blocks.size());
       w.num_qblk = (int32_t)blocks.size();
+      w.num_seg = ns_total - w.seg_begin;
       nq_total += w.num_qblk;
     }
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -640,6 +750,24 @@ kv_status kv_rebuild_stage(kv_arena_t arena, const int32_t* tokens, const int32_
   }
   *out = plan;
   return ok();
+}
+
+}  // namespace
+
+kv_status kv_rebuild_stage(kv_arena_t arena, const int32_t* tokens, const int32_t* lens, int32_t R,
+                           const int32_t* tables, int32_t max_blocks, void* workspace,
+                           uint64_t ws_bytes, void* stream, kv_plan_t* out) {
+  return stage_impl(arena, tokens, lens, nullptr, R, tables, max_blocks, workspace, ws_bytes, stream,
+                    out);
+}
+
+kv_status kv_rebuild_stage_from(kv_arena_t arena, const int32_t* tokens, const int32_t* lens,
+                                const int32_t* starts, int32_t R, const int32_t* tables,
+                                int32_t max_blocks, void* workspace, uint64_t ws_bytes, void* stream,
+                                kv_plan_t* out) {
+  if (R > 0 && !starts) return fail(KV_EINVAL, "null starts");
+  return stage_impl(arena, tokens, lens, starts, R, tables, max_blocks, workspace, ws_bytes, stream,
+                    out);
 }
 
 kv_status kv_plan_release(kv_plan_t plan) {
@@ -713,7 +841,10 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
     const int32_t* tok = reinterpret_cast<const int32_t*>(ws + L.tok) + wv.tok_begin;
     const int32_t* pos = reinterpret_cast<const int32_t*>(ws + L.pos) + wv.tok_begin;
     const int64_t* slot = reinterpret_cast<const int64_t*>(ws + L.slot) + wv.tok_begin;
+    const int32_t* krow = plan->has_prefix ? reinterpret_cast<const int32_t*>(ws + L.krow) + wv.tok_begin : nullptr;
+    const int64_t* kslot = reinterpret_cast<const int64_t*>(ws + L.kslot) + wv.key_begin;
     const int4* qblk = reinterpret_cast<const int4*>(ws + L.qblk) + wv.qblk_begin;
+    const int2* segs = reinterpret_cast<const int2*>(ws + L.seg) + wv.seg_begin;
     {
       ProfScope ps(ar, s, KV_PROF_NORM, 0.0);
       launch_embed_norm(dt, w->embed, tok, w->layers[0].attn_norm, X, A, M, H, eps, s);
@@ -746,7 +877,8 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
       g.epi.arena_v = plane_v;
       g.epi.vt = VT;
       g.epi.kc = KC;
-      g.epi.ldvt = L.Wpad;
+      g.epi.ldvt = L.Wkpad;
+      g.epi.krow = krow;
       g.epi.slot = slot;
       g.epi.pos = pos;
       g.epi.rope = rope;
@@ -764,6 +896,11 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
         gemm(EPI_QKV, g, s);
       }
       if (last) break;
+      if (wv.num_seg > 0 && dt == KV_BF16) {
+        // retained prefix keys of this layer into the K copy and V^T
+        ProfScope ps(ar, s, KV_PROF_ATTN, 0.0);
+        launch_prefix_gather(segs, wv.num_seg, kslot, plane_k, plane_v, KC, VT, L.Wkpad, nkv, hd, s);
+      }
 
       AttnParams ap{};
       ap.q = Q;
@@ -771,8 +908,8 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
       ap.arena_v = plane_v;
       ap.vt = VT;
       ap.kc = KC;
-      ap.ldvt = L.Wpad;
-      ap.slot = slot;
+      ap.ldvt = L.Wkpad;
+      ap.kslot = kslot;
       ap.qblk = qblk;
       ap.num_qblk = wv.num_qblk;
       ap.out = U;
@@ -840,6 +977,36 @@ kv_status kv_rebuild_execute(const kv_weights* w, kv_plan_t plan, void* stream) 
   }
   const hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(KV_EDEVICE, "kernel launch failed: %s", hipGetErrorString(err));
+  return ok();
+}
+
+kv_status kv_rebuild_from_check(const kv_model_desc* desc, int32_t block_size, int64_t num_blocks,
+                                const int32_t* tokens, const int32_t* lens, const int32_t* starts,
+                                int32_t num_requests, const int32_t* block_tables,
+                                int32_t max_blocks_per_req) {
+  if (num_requests > 0 && !starts) return fail(KV_EINVAL, "null starts");
+  kv_status st = check_request(desc, block_size, num_blocks, tokens, lens, num_requests, block_tables,
+                               max_blocks_per_req, nullptr, nullptr, starts);
+  return st == KV_OK ? ok() : st;
+}
+
+kv_status kv_rebuild_from(const kv_weights* w, const int32_t* tokens, const int32_t* lens,
+                          const int32_t* starts, int32_t R, const int32_t* tables, int32_t max_blocks,
+                          kv_arena_t arena, void* workspace, uint64_t ws_bytes, void* stream) {
+  if (!w) return fail(KV_EINVAL, "null weights");
+  if (!live_arena(arena)) return fail(KV_ESTATE, "unknown or released arena handle");
+  if (!same_desc(w->desc, arena->desc)) return fail(KV_ESTATE, "weights and arena describe different models");
+  kv_plan_t plan = nullptr;
+  kv_status st = kv_rebuild_stage_from(arena, tokens, lens, starts, R, tables, max_blocks, workspace,
+                                       ws_bytes, stream, &plan);
+  if (st != KV_OK) return st;
+  st = kv_rebuild_execute(w, plan, stream);
+  const std::string keep = g_err;
+  kv_plan_release(plan);
+  if (st != KV_OK) {
+    g_err = keep;
+    return st;
+  }
   return ok();
 }
 

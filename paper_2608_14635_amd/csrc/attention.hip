@@ -84,8 +84,8 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   bid -= qb * p.nkv * ngrp;
   const int kvh = bid / ngrp, hgrp = bid % ngrp;
   const int4 blk = p.qblk[qb];
-  const int q_start = blk.x, q_len = blk.y, req_start = blk.z;
-  const int nkeys = q_start + q_len - req_start;
+  const int q_start = blk.x, q_len = blk.y, key_base = blk.z, pos0 = blk.w;
+  const int nkeys = pos0 + q_len;
   const int ntiles = (nkeys + KB - 1) / KB;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -94,9 +94,9 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   const int half = lane >> 5, col = lane & 31;
   const bool wave_active = qsub * 32 < q_len;
   const int qi = min(qsub * 32 + col, q_len - 1);            // clamped query of this lane
-  const int qpos = q_start + qi - req_start;                 // its position in the request
-  const int wave_first = q_start + qsub * 32 - req_start;
-  const int wave_last = q_start + min(qsub * 32 + 31, q_len - 1) - req_start;
+  const int qpos = pos0 + qi;                                // its position in the request
+  const int wave_first = pos0 + qsub * 32;
+  const int wave_last = pos0 + min(qsub * 32 + 31, q_len - 1);
 
   const int ldq = p.nq * D;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(p.q);
@@ -144,12 +144,12 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   }
   // key offset (within a 32-key half) of accumulator register r: ksig(8*(r/4) + 4*half + r%4)
 
-  issue_kv(smem, Kc, Vt, head_bytes, req_start, 0, wid, k_voff, v_voff);
-  issue_kv(smem, Kc, Vt, head_bytes, req_start + min(1, ntiles - 1) * KB, 1, wid, k_voff, v_voff);
+  issue_kv(smem, Kc, Vt, head_bytes, key_base, 0, wid, k_voff, v_voff);
+  issue_kv(smem, Kc, Vt, head_bytes, key_base + min(1, ntiles - 1) * KB, 1, wid, k_voff, v_voff);
   for (int kt = 0; kt < ntiles; ++kt) {
     KVR_WAIT_VMCNT(4);                      // this wave's loads of tile kt have landed
     __builtin_amdgcn_s_barrier();           // ... and every other wave's; stage of kt-1 is free
-    issue_kv(smem, Kc, Vt, head_bytes, req_start + min(kt + 2, ntiles - 1) * KB, (kt + 2) % NSTAGE,
+    issue_kv(smem, Kc, Vt, head_bytes, key_base + min(kt + 2, ntiles - 1) * KB, (kt + 2) % NSTAGE,
              wid, k_voff, v_voff);
     const char* st = smem + (kt % NSTAGE) * STAGE;
 
@@ -286,7 +286,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
   const int qb = blockIdx.x / p.nq, h = blockIdx.x % p.nq;
   const int kvh = h / (p.nq / p.nkv);
   const int4 blk = p.qblk[qb];
-  const int q_start = blk.x, q_len = blk.y, req_start = blk.z;
+  const int q_start = blk.x, q_len = blk.y, key_base = blk.z, pos0 = blk.w;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int d = p.d;
   const float scale = 1.0f / sqrtf((float)d);
@@ -303,8 +303,8 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
       q[t] = e < d ? Q[(int64_t)tq * ldq + h * d + e] : 0.0f;
     }
     float m = -INFINITY, l = 0.0f;
-    for (int tk = req_start; tk <= tq; ++tk) {
-      const int64_t row = (p.slot[tk] * p.nkv + kvh) * (int64_t)d;
+    for (int j = 0; j <= pos0 + qi; ++j) {
+      const int64_t row = (p.kslot[key_base + j] * p.nkv + kvh) * (int64_t)d;
       float part = 0.0f;
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
@@ -330,7 +330,50 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
   }
 }
 
+// Prefix keys of a rebuild from a retained prefix, for the bf16 kernel above:
+// workgroup (segment, kv head) copies up to 64 keys' K rows from the arena
+// into the K copy and their V rows, through LDS, into V^T (8 consecutive
+// keys of one dim per 16-byte store; segments start on a multiple of 8 key
+// rows and hold a multiple of 8 keys).
+__global__ __launch_bounds__(256) void prefix_gather_kernel(const int2* segs, const int64_t* kslot,
+                                                            const bf16_t* plane_k,
+                                                            const bf16_t* plane_v, bf16_t* kc,
+                                                            bf16_t* vt, int64_t ldvt, int nkv) {
+  constexpr int GP = D + 8;  // LDS pitch, elements
+  __shared__ __attribute__((aligned(16))) uint16_t sv[GATHER_KEYS * GP];
+  const int seg = blockIdx.x / nkv, h = blockIdx.x % nkv;
+  const int2 sg = segs[seg];
+  const int kr0 = sg.x, cnt = sg.y;
+  const int tid = threadIdx.x;
+  const int64_t row_elems = (int64_t)nkv * D;
+  for (int it = tid; it < cnt * (D / 8); it += 256) {
+    const int k = it / (D / 8), u = it % (D / 8);
+    const int64_t src = kslot[kr0 + k] * row_elems + (int64_t)h * D + u * 8;
+    *reinterpret_cast<uint4*>(kc + ((int64_t)h * ldvt + kr0 + k) * D + u * 8) =
+        *reinterpret_cast<const uint4*>(plane_k + src);
+    *reinterpret_cast<uint4*>(sv + k * GP + u * 8) = *reinterpret_cast<const uint4*>(plane_v + src);
+  }
+  __syncthreads();
+  for (int it = tid; it < D * (cnt / 8); it += 256) {
+    const int e = it % D, k8 = (it / D) * 8;
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = (uint32_t)sv[(k8 + 2 * i) * GP + e] | ((uint32_t)sv[(k8 + 2 * i + 1) * GP + e] << 16);
+    *reinterpret_cast<uint4*>(vt + ((int64_t)h * D + e) * ldvt + kr0 + k8) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
 }  // namespace
+
+void launch_prefix_gather(const int2* segs, int nseg, const int64_t* kslot, const void* plane_k,
+                          const void* plane_v, void* kc, void* vt, int64_t ldvt, int nkv, int d,
+                          hipStream_t s) {
+  if (nseg <= 0 || d != D) return;
+  hipLaunchKernelGGL(prefix_gather_kernel, dim3((unsigned)(nseg * nkv)), dim3(256), 0, s, segs, kslot,
+                     reinterpret_cast<const bf16_t*>(plane_k), reinterpret_cast<const bf16_t*>(plane_v),
+                     reinterpret_cast<bf16_t*>(kc), reinterpret_cast<bf16_t*>(vt), ldvt, nkv);
+}
 
 void launch_attention_bf16(const AttnParams& p, hipStream_t s) {
   if (p.num_qblk <= 0) return;

@@ -109,7 +109,8 @@ __device__ __forceinline__ void epi_qkv(float* sC, int ldc, int rows, int m_base
         if (e.kc != nullptr) {
           // contiguous per-head copy for attention; padding rows hold zeros so
           // that keys past a request's end are inert whatever their residual holds
-          T* kd = reinterpret_cast<T*>(e.kc) + ((int64_t)kh * e.ldvt + m) * d;
+          const int64_t kr = e.krow != nullptr ? e.krow[m] : m;
+          T* kd = reinterpret_cast<T*>(e.kc) + ((int64_t)kh * e.ldvt + kr) * d;
           if (sl < 0) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) lo[i] = hi[i] = 0.0f;
@@ -150,8 +151,10 @@ __device__ __forceinline__ void epi_qkv(float* sC, int ldc, int rows, int m_base
       store8(dst, v);
     }
     if (e.vt != nullptr) {
-      // V^T[col][m]: 8 consecutive rows of one column per item; padding rows
-      // get zeros, so attention reads inert values past a request's last key
+      // V^T[col][krow(m)]: 8 consecutive rows of one column per item (their key
+      // rows are consecutive too: a request's rows start on a multiple of 8,
+      // and so do its suffix key rows); padding rows get zeros, so attention
+      // reads inert values past a request's last key
       const int rchunks = rows / 8;
       for (int it = tid; it < BN * rchunks; it += NT) {
         const int c = it % BN, rc = it / BN;
@@ -161,7 +164,8 @@ __device__ __forceinline__ void epi_qkv(float* sC, int ldc, int rows, int m_base
         float v[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) v[i] = e.slot[m0 + i] < 0 ? 0.0f : src[(int64_t)i * ldc];
-        store8(reinterpret_cast<T*>(e.vt) + (int64_t)(vbase + c) * e.ldvt + m0, v);
+        const int64_t kr0 = e.krow != nullptr ? e.krow[m0] : m0;
+        store8(reinterpret_cast<T*>(e.vt) + (int64_t)(vbase + c) * e.ldvt + kr0, v);
       }
     }
   }

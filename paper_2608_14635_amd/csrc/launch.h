@@ -26,9 +26,10 @@ struct EpiParams {
   void* q_out;            // [rows][nq*d]
   void* arena_k;          // this layer's K plane: [slots][nkv][d]
   void* arena_v;          // this layer's V plane
-  void* vt;               // V^T [nkv*d][ldvt] (bf16 path) or null; row m at column m
+  void* vt;               // V^T [nkv*d][ldvt] (bf16 path) or null; row m at column krow(m)
   int64_t ldvt;
-  void* kc;               // K copy [nkv][ldvt][d] (bf16 path) or null; row m at row m
+  void* kc;               // K copy [nkv][ldvt][d] (bf16 path) or null; row m at row krow(m)
+  const int32_t* krow;    // per row: its key row in kc/vt (null = the row itself)
   const int64_t* slot;    // per wave-local row: arena slot index, -1 for padding rows
   const int32_t* pos;     // per wave-local token: position within its request
   const float2* rope;     // [max_pos][d/2] (cos, sin)
@@ -91,6 +92,11 @@ int64_t gemm_bf16_splitk_part_elems(int M, int N, int K);
 // Attention.  qblk: per q-block int4 {q_start, q_len, req_start, 0} in
 // wave-local row indices, ordered longest-first.  Each request's rows start on
 // a ROW_ALIGN boundary; the padding rows after it hold finite values.
+// A q-block is (first query row, query count, key row of position 0 of its
+// request, position of the first query): its queries attend key rows
+// key_base .. key_base + position.  Query rows and key rows are separate
+// index spaces (a rebuild from a retained prefix has key rows for the
+// prefix but no query rows); they coincide when every request starts at 0.
 struct AttnParams {
   const void* q;          // [rows][nq*d]
   const void* arena_k;    // this layer's K plane
@@ -98,7 +104,7 @@ struct AttnParams {
   const void* vt;         // V^T [nkv*d][ldvt] (bf16 path)
   int64_t ldvt;
   const void* kc;         // K copy [nkv][ldvt][d] (bf16 path)
-  const int64_t* slot;
+  const int64_t* kslot;   // per key row: arena slot (fp32 path reads the arena)
   const int4* qblk;
   int num_qblk;
   void* out;              // [rows][nq*d]
@@ -115,6 +121,13 @@ inline int attn_qblock(int dtype, int group) {
 constexpr int ATTN_QBLOCK_MIN = 32;
 constexpr int ROW_ALIGN = 64;  // each request's rows start on this boundary of the wave
 void launch_attention_bf16(const AttnParams& p, hipStream_t s);
+// Prefix keys of a rebuild from a retained prefix: segment (key row, count
+// <= 64) copies the arena K/V of those key rows' slots into the K copy and
+// V^T (bf16 path).
+constexpr int GATHER_KEYS = 64;
+void launch_prefix_gather(const int2* segs, int nseg, const int64_t* kslot, const void* plane_k,
+                          const void* plane_v, void* kc, void* vt, int64_t ldvt, int nkv, int d,
+                          hipStream_t s);
 void launch_attention_f32(const AttnParams& p, int rows_total, hipStream_t s);
 
 // Resumed decode (one token per request over the paged arena).

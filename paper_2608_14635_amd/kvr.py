@@ -1,5 +1,5 @@
 """Thin ctypes binding of libkvr.so (include/kvr.h, include/kvr_decode.h,
-include/kvr_ipc.h, include/kvr_verify.h, include/kvr_profile.h).
+include/kvr_ipc.h, include/kvr_verify.h, include/kvr_reuse.h, include/kvr_profile.h).
 
 Argument marshalling only: every step of the rebuild runs in the library's
 HIP kernels.  Device buffers are passed as integer addresses (for example a
@@ -102,6 +102,18 @@ def lib() -> C.CDLL:
     L.kv_decode_step.restype = C.c_int
     L.kv_decode_step.argtypes = [C.POINTER(kv_weights), vp, vp, i32p, i32p, C.c_int32, i32p,
                                  C.c_int32, vp, vp, C.c_uint64, vp, vp, vp]
+    L.kv_rebuild_from_workspace_bytes.restype = C.c_uint64
+    L.kv_rebuild_from_workspace_bytes.argtypes = [C.POINTER(kv_model_desc), C.c_int32, C.c_int64,
+                                                  C.c_int64, C.c_int64]
+    L.kv_rebuild_from_check.restype = C.c_int
+    L.kv_rebuild_from_check.argtypes = [C.POINTER(kv_model_desc), C.c_int32, C.c_int64, i32p, i32p,
+                                        i32p, C.c_int32, i32p, C.c_int32]
+    L.kv_rebuild_from.restype = C.c_int
+    L.kv_rebuild_from.argtypes = [C.POINTER(kv_weights), i32p, i32p, i32p, C.c_int32, i32p, C.c_int32,
+                                  vp, vp, C.c_uint64, vp]
+    L.kv_rebuild_stage_from.restype = C.c_int
+    L.kv_rebuild_stage_from.argtypes = [vp, i32p, i32p, i32p, C.c_int32, i32p, C.c_int32, vp,
+                                        C.c_uint64, vp, C.POINTER(vp)]
     L.kv_verify_workspace_bytes.restype = C.c_uint64
     L.kv_verify_workspace_bytes.argtypes = [C.c_int32, C.c_int64]
     L.kv_block_digests.restype = C.c_int
@@ -235,6 +247,44 @@ def kv_plan_info(plan: int) -> Tuple[int, int]:
     return nw.value, mx.value
 
 
+def kv_rebuild_from_workspace_bytes(shape_or_desc, num_requests: int, total_rows: int,
+                                    total_keys: int, wave_rows: int) -> int:
+    d = shape_or_desc if isinstance(shape_or_desc, kv_model_desc) else make_desc(shape_or_desc)
+    return int(lib().kv_rebuild_from_workspace_bytes(C.byref(d), num_requests, total_rows, total_keys,
+                                                     wave_rows))
+
+
+def kv_rebuild_from_check(shape_or_desc, block_size: int, num_blocks: int, tokens, lens, starts,
+                          tables) -> int:
+    """Host-only validation of a rebuild from retained prefixes; the status code."""
+    d = shape_or_desc if isinstance(shape_or_desc, kv_model_desc) else make_desc(shape_or_desc)
+    tok, ln, st = _i32(tokens), _i32(lens), _i32(starts)
+    tab, mb = _tables2d(tables, len(ln))
+    return int(lib().kv_rebuild_from_check(C.byref(d), block_size, num_blocks, _ptr(tok), _ptr(ln),
+                                           _ptr(st), len(ln), _ptr(tab), mb))
+
+
+def kv_rebuild_from(weights: Weights, tokens, lens, starts, tables, arena: int, workspace: int,
+                    workspace_bytes: int, stream: int = 0) -> None:
+    """Recompute positions starts[r] .. lens[r]-1; tokens are those positions' tokens only."""
+    tok, ln, st = _i32(tokens), _i32(lens), _i32(starts)
+    tab, mb = _tables2d(tables, len(ln))
+    _check(lib().kv_rebuild_from(C.byref(weights.c), _ptr(tok), _ptr(ln), _ptr(st), len(ln), _ptr(tab),
+                                 mb, C.c_void_p(arena), C.c_void_p(workspace), workspace_bytes,
+                                 C.c_void_p(stream)))
+
+
+def kv_rebuild_stage_from(arena: int, tokens, lens, starts, tables, workspace: int,
+                          workspace_bytes: int, stream: int = 0) -> int:
+    tok, ln, st = _i32(tokens), _i32(lens), _i32(starts)
+    tab, mb = _tables2d(tables, len(ln))
+    plan = C.c_void_p()
+    _check(lib().kv_rebuild_stage_from(C.c_void_p(arena), _ptr(tok), _ptr(ln), _ptr(st), len(ln),
+                                       _ptr(tab), mb, C.c_void_p(workspace), workspace_bytes,
+                                       C.c_void_p(stream), C.byref(plan)))
+    return plan.value
+
+
 def kv_decode_workspace_bytes(shape_or_desc, num_requests: int, max_position: int) -> int:
     d = shape_or_desc if isinstance(shape_or_desc, kv_model_desc) else make_desc(shape_or_desc)
     return int(lib().kv_decode_workspace_bytes(C.byref(d), num_requests, max_position))
@@ -351,4 +401,6 @@ def exported_symbols() -> Iterable[str]:
             "kv_plan_info", "kv_last_error", "kv_profile_enable", "kv_profile_read",
             "kv_profile_reset", "kv_decode_workspace_bytes", "kv_decode_check", "kv_decode_step",
             "kv_ipc_export", "kv_ipc_owner_alive", "kv_ipc_open", "kv_ipc_close",
-            "kv_verify_workspace_bytes", "kv_block_digests", "kv_verify")
+            "kv_verify_workspace_bytes", "kv_block_digests", "kv_verify",
+            "kv_rebuild_from_workspace_bytes", "kv_rebuild_from_check", "kv_rebuild_from",
+            "kv_rebuild_stage_from")

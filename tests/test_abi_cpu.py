@@ -308,3 +308,54 @@ def test_verify_rejects_unknown_arena_and_null_records(L):
     with pytest.raises(kvr.KvError) as e:
         kvr.kv_verify(0x1234, lens, tables, 0x4000, 0x10000, 1 << 20, 0x3000)
     assert e.value.status == kvr.KV_ESTATE
+
+
+def _from_valid(B=16):
+    shape = W.TINY_BF16
+    lens = np.array([40, 64, 0, 17], np.int32)
+    starts = np.array([32, 16, 0, 8], np.int32)
+    NB = 20
+    rng = np.random.default_rng(3)
+    tables = np.full((4, 4), -1, np.int32)
+    nxt = 0
+    for r, n in enumerate(lens):
+        for j in range((n + B - 1) // B):
+            tables[r, j] = nxt
+            nxt += 1
+    toks = rng.integers(0, shape.vocab, size=int((lens - starts).sum())).astype(np.int32)
+    return shape, toks, lens, starts, tables, B, NB
+
+
+def test_rebuild_from_workspace_bytes(L):
+    s = W.LLAMA8B
+    a = kvr.kv_rebuild_from_workspace_bytes(s, 4, 1000, 1000, 1000)
+    b = kvr.kv_rebuild_from_workspace_bytes(s, 4, 1000, 9000, 1000)
+    assert 0 < a < b
+    assert kvr.kv_rebuild_from_workspace_bytes(s, 4, 1000, 999, 1000) == 0
+    # with no prefix it sizes like the plain rebuild's workspace at one wave
+    assert a >= kvr.kv_rebuild_workspace_bytes(s, 4, 1000, 1000)
+
+
+def test_rebuild_from_check(L):
+    shape, toks, lens, starts, tables, B, NB = _from_valid()
+    assert kvr.kv_rebuild_from_check(shape, B, NB, toks, lens, starts, tables) == kvr.KV_OK
+    # starts = 0 is the plain rebuild's check
+    full = np.concatenate([np.arange(n) % shape.vocab for n in lens]).astype(np.int32)
+    assert kvr.kv_rebuild_from_check(shape, B, NB, full, lens, np.zeros(4, np.int32), tables) == kvr.KV_OK
+    assert kvr.kv_rebuild_check(shape, B, NB, full, lens, tables) == kvr.KV_OK
+    bad = starts.copy(); bad[0] = 41          # past the length
+    assert kvr.kv_rebuild_from_check(shape, B, NB, toks, lens, bad, tables) == kvr.KV_EINVAL
+    bad = starts.copy(); bad[1] = 12          # not a multiple of 8
+    assert kvr.kv_rebuild_from_check(shape, B, NB, toks, lens, bad, tables) == kvr.KV_EINVAL
+    bad = starts.copy(); bad[3] = 17          # = length: nothing to compute, any value allowed
+    assert kvr.kv_rebuild_from_check(shape, B, NB, toks[:-9], lens, bad, tables) == kvr.KV_OK
+    # a prefix block may be shared read-only, also with an earlier writer
+    t = tables.copy(); t[1, 0] = tables[0, 0]  # request 1 reads request 0's first block
+    assert kvr.kv_rebuild_from_check(shape, B, NB, toks, lens, starts, t) == kvr.KV_OK
+    t = tables.copy(); t[0, 0] = tables[3, 1]  # request 0 reads what request 3 writes later
+    assert kvr.kv_rebuild_from_check(shape, B, NB, toks, lens, starts, t) == kvr.KV_EALIAS
+    t = tables.copy(); t[1, 1] = tables[0, 2]  # two writers
+    assert kvr.kv_rebuild_from_check(shape, B, NB, toks, lens, starts, t) == kvr.KV_EALIAS
+    t = tables.copy(); t[0, 0] = NB            # out of range, read-only block included
+    assert kvr.kv_rebuild_from_check(shape, B, NB, toks, lens, starts, t) == kvr.KV_ERANGE
+    assert L.kv_rebuild_from_check(C.byref(kvr.make_desc(shape)), B, NB, None, None, None, 1, None, 4) == kvr.KV_EINVAL
