@@ -466,7 +466,9 @@ uint64_t kv_rebuild_from_workspace_bytes(const kv_model_desc* desc, int32_t num_
   const int64_t pad = (int64_t)(ROW_ALIGN - 1) * num_requests;
   const int64_t Tg = total_rows + pad, Tk = total_keys + 2 * pad;
   const int64_t W = std::min(wave_rows, total_rows) + pad;
-  const int64_t nseg = (total_keys - total_rows) / GATHER_KEYS + num_requests + 1;
+  // gather segments: the prefixes in pieces of GATHER_KEYS, plus at most
+  // one partial piece and one zero-fill segment per request
+  const int64_t nseg = (total_keys - total_rows) / GATHER_KEYS + 2 * (int64_t)num_requests + 1;
   return make_layout(*desc, num_requests, Tg, W, Tk, key_capacity(W, Tg, Tk, 0), nseg).total;
 }
 
@@ -608,7 +610,7 @@ kv_status stage_impl(kv_arena_t arena, const int32_t* tokens, const int32_t* len
       gmax = std::max(gmax, g);
       kmax = std::max(kmax, k);
       if (n > 0 && st0[r] > 0) {
-        nseg += (st0[r] + GATHER_KEYS - 1) / GATHER_KEYS;
+        nseg += (st0[r] + GATHER_KEYS - 1) / GATHER_KEYS + (k > st0[r] + g ? 1 : 0);
         plan->has_prefix = true;
       }
     }
@@ -723,8 +725,14 @@ kv_status stage_impl(kv_arena_t arena, const int32_t* tokens, const int32_t* len
         const int32_t rs = (int32_t)(row_off[r] - w.tok_begin), ks = (int32_t)(key_off[r] - w.key_begin);
         for (int32_t qs = 0; qs < n; qs += QB)
           blocks.push_back(make_int4(rs + qs, std::min(QB, n - qs), ks, st0[r] + qs));
+        if (n == 0 || st0[r] == 0) continue;
         for (int32_t p0 = 0; p0 < st0[r]; p0 += GATHER_KEYS)
           hseg[ns_total++] = make_int2(ks + p0, std::min(GATHER_KEYS, st0[r] - p0));
+        // key rows past the computed ones up to the 64-aligned region end:
+        // zeros (a negative count), since the last key tile reads them
+        const int32_t kend = st0[r] + (int32_t)(row_off[r + 1] - row_off[r]);
+        const int32_t ktot = (int32_t)(key_off[r + 1] - key_off[r]);
+        if (ktot > kend) hseg[ns_total++] = make_int2(ks + kend, -(ktot - kend));
       }
       // longest causal extent first
       std::stable_sort(blocks.begin(), blocks.end(),

@@ -334,7 +334,10 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
 // workgroup (segment, kv head) copies up to 64 keys' K rows from the arena
 // into the K copy and their V rows, through LDS, into V^T (8 consecutive
 // keys of one dim per 16-byte store; segments start on a multiple of 8 key
-// rows and hold a multiple of 8 keys).
+// rows).  A segment with a negative count instead writes zeros to -count key
+// rows (a multiple of 8): the rows between a request's last computed row and
+// the end of its 64-aligned key region, which the last key tile reads and
+// which must be finite since masked probabilities multiply them.
 __global__ __launch_bounds__(256) void prefix_gather_kernel(const int2* segs, const int64_t* kslot,
                                                             const bf16_t* plane_k,
                                                             const bf16_t* plane_v, bf16_t* kc,
@@ -345,6 +348,15 @@ __global__ __launch_bounds__(256) void prefix_gather_kernel(const int2* segs, co
   const int2 sg = segs[seg];
   const int kr0 = sg.x, cnt = sg.y;
   const int tid = threadIdx.x;
+  if (cnt < 0) {  // uniform over the workgroup
+    const int z = -cnt;
+    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+    for (int it = tid; it < z * (D / 8); it += 256)
+      *reinterpret_cast<uint4*>(kc + ((int64_t)h * ldvt + kr0 + it / (D / 8)) * D + (it % (D / 8)) * 8) = zero;
+    for (int it = tid; it < D * (z / 8); it += 256)
+      *reinterpret_cast<uint4*>(vt + ((int64_t)h * D + it % D) * ldvt + kr0 + (it / D) * 8) = zero;
+    return;
+  }
   const int64_t row_elems = (int64_t)nkv * D;
   for (int it = tid; it < cnt * (D / 8); it += 256) {
     const int k = it / (D / 8), u = it % (D / 8);

@@ -305,9 +305,13 @@ class DeviceArena:
 
 
 def alloc_workspace(shape: W.ModelShape, num_requests: int, total_tokens: int,
-                    wave_tokens: int, device="cuda"):
+                    wave_tokens: int, device="cuda", fill=None):
+    """A rebuild workspace; `fill` (a byte value) overwrites its contents
+    first, e.g. 0xFF so that any read of a never-written element yields NaN."""
     nbytes = kvr.kv_rebuild_workspace_bytes(shape, num_requests, total_tokens, wave_tokens)
     ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+    if fill is not None:
+        ws.fill_(fill)
     return ws, nbytes
 
 

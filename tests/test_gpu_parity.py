@@ -57,7 +57,7 @@ def gpu_rebuild(wl, model, host_image=None, wave_tokens=None, arena=None):
         arena.bind()
     T = wl.total_tokens
     wt = wave_tokens or max(T, 1)
-    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, T, wt)
+    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, T, wt, fill=0xFF)
     kvr.kv_rebuild(model.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle,
                    ws.data_ptr(), nbytes, Hn.stream_ptr())
     torch.cuda.synchronize()
@@ -158,7 +158,7 @@ def test_stage_execute_matches_rebuild(tiny_bf16):
     model = Hn.device_model_from_host(wl.shape, host_w)
     arena = Hn.DeviceArena(wl, host_image=image)
     arena.bind()
-    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, wl.total_tokens, wl.total_tokens)
+    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, wl.total_tokens, wl.total_tokens, fill=0xFF)
     say("stage once, execute twice")
     plan = kvr.kv_rebuild_stage(arena.handle, wl.tokens, wl.lens, wl.block_tables, ws.data_ptr(),
                                 nbytes, Hn.stream_ptr())
@@ -180,7 +180,7 @@ def test_errors_leave_arena_untouched(tiny_bf16):
     model = Hn.device_model_from_host(wl.shape, host_w)
     arena = Hn.DeviceArena(wl, host_image=image)
     arena.bind()
-    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, wl.total_tokens, wl.total_tokens)
+    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, wl.total_tokens, wl.total_tokens, fill=0xFF)
     before = arena.bits.clone()
     cases = []
     t = wl.tokens.copy(); t[3] = wl.shape.vocab; cases.append(("token", t, wl.lens, wl.block_tables, kvr.KV_ERANGE))
@@ -286,7 +286,7 @@ def test_full_config2_sampled_layer0_and_invariants(oracle_lib):
     model = Hn.device_model_random(wl.shape, seed=2)
     arena = Hn.DeviceArena(wl)
     arena.bind()
-    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, wl.total_tokens, wl.total_tokens)
+    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, wl.total_tokens, wl.total_tokens, fill=0xFF)
     kvr.kv_rebuild(model.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle,
                    ws.data_ptr(), nbytes, Hn.stream_ptr())
     torch.cuda.synchronize()

@@ -20,6 +20,10 @@ import parity_util as PU  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 LLAMA8B_2L = W.LLAMA8B.with_layers(2)
+# workspaces start as all-ones bytes (NaN in bf16 and fp32), so that a read of
+# an element no kernel wrote shows up as a non-finite result, whatever the
+# caching allocator handed back
+POISON = 0xFF
 
 
 def say(msg):
@@ -45,7 +49,7 @@ def gpu_from(model, wl, arena, tokens, lens, starts, tables):
     rows = int((np.asarray(lens) - np.asarray(starts)).sum())
     keys = int(np.asarray(lens).sum())
     nbytes = kvr.kv_rebuild_from_workspace_bytes(wl.shape, len(lens), rows, keys, max(rows, 1))
-    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda").fill_(POISON)
     kvr.kv_rebuild_from(model.weights, tokens, lens, starts, tables, arena.handle, ws.data_ptr(),
                         nbytes, Hn.stream_ptr())
     torch.cuda.synchronize()
@@ -53,7 +57,7 @@ def gpu_from(model, wl, arena, tokens, lens, starts, tables):
 
 def gpu_full(model, wl, arena, tokens, lens, tables):
     T = int(np.asarray(lens).sum())
-    ws, nbytes = Hn.alloc_workspace(wl.shape, len(lens), T, max(T, 1))
+    ws, nbytes = Hn.alloc_workspace(wl.shape, len(lens), T, max(T, 1), fill=POISON)
     kvr.kv_rebuild(model.weights, tokens, lens, tables, arena.handle, ws.data_ptr(), nbytes,
                    Hn.stream_ptr())
     torch.cuda.synchronize()
