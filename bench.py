@@ -147,16 +147,24 @@ def flush_free(wl, model, arena, ws_rebuild, Hn, kvr, reps, stream, log):
     all_intact = bool(np.array_equal(intact[:R].cpu().numpy(), nb))
     covered = int(wl.lens.astype(np.int64).sum()) * s.num_layers * 2 * s.num_kv_heads * s.head_dim * s.elem_bytes
     moved = covered + 8 * E + E + 4 * (R + 1) + 8 * E + 4 * R
-    # one damaged request (the median-length one): verify, then rebuild it alone
+    # one damaged request (the median-length one), damaged in its middle block:
+    # (a) verify, then rebuild that request alone; (b) verify, then rebuild it
+    # from its first damaged block, rounded down to a multiple of 256
+    # positions (where the recomputed values are the full rebuild's bit for
+    # bit, so the committed digests stay valid)
     r = int(np.argsort(wl.lens)[R // 2])
     blk = int(wl.block_tables[r, int(nb[r]) // 2])
-    arena.bits[s.num_layers - 1, 1, blk, 0, 0, 0] ^= 1
-    torch.cuda.synchronize()
+    offs = wl.request_offsets()
+
+    def damage():
+        arena.bits[s.num_layers - 1, 1, blk, 0, 0, 0] ^= 1
+        torch.cuda.synchronize()
+
+    damage()
     t0 = time.perf_counter()
     verify()
     got = intact[:R].cpu().numpy()
     bad = np.nonzero(got < nb)[0]
-    offs = wl.request_offsets()
     toks = np.concatenate([wl.tokens[offs[i]:offs[i] + wl.lens[i]] for i in bad]) if bad.size else \
         np.zeros(0, np.int32)
     kvr.kv_rebuild(model.weights, toks, wl.lens[bad], wl.block_tables[bad], arena.handle,
@@ -165,15 +173,73 @@ def flush_free(wl, model, arena, ws_rebuild, Hn, kvr, reps, stream, log):
     rec_ms = (time.perf_counter() - t0) * 1e3
     verify()
     healed = bool(np.array_equal(intact[:R].cpu().numpy(), nb))
+    damage()
+    t0 = time.perf_counter()
+    verify()
+    got = intact[:R].cpu().numpy()
+    bad = np.nonzero(got < nb)[0]
+    starts = ((got[bad] * B) // 256 * 256).astype(np.int32)
+    toks = np.concatenate([wl.tokens[offs[i] + st:offs[i] + wl.lens[i]] for i, st in zip(bad, starts)]) \
+        if bad.size else np.zeros(0, np.int32)
+    kvr.kv_rebuild_from(model.weights, toks, wl.lens[bad], starts, wl.block_tables[bad], arena.handle,
+                        ws_rebuild[0].data_ptr(), ws_rebuild[1], stream)
+    torch.cuda.synchronize()
+    from_ms = (time.perf_counter() - t0) * 1e3
+    verify()
+    healed_from = bool(np.array_equal(intact[:R].cpu().numpy(), nb))
     out = {"entries": E, "verify_ms": ms, "covered_bytes": covered, "bytes_per_launch": moved,
            "achieved_GBps": moved / (ms / 1e3) / 1e9, "hbm_frac": moved / (ms / 1e3) / 1e9 / PEAK_HBM_GBS,
            "traffic": measured_traffic("verify", wl.name), "source_sha": kernel_source_hash("verify"),
            "all_intact_after_rebuild": all_intact,
            "one_damaged_request": {"request": r, "tokens": int(wl.lens[r]),
                                    "detected": bad.tolist(), "recovery_ms": rec_ms,
-                                   "intact_after": healed}}
+                                   "intact_after": healed,
+                                   "from_position": int(starts[0]) if bad.size else None,
+                                   "recovery_from_block_ms": from_ms,
+                                   "intact_after_from_block": healed_from}}
     log(f"[bench] verify scan: {ms:.3f} ms over {E} blocks, {out['achieved_GBps']:.0f} GB/s "
-        f"({100 * out['hbm_frac']:.1f}% of HBM); one damaged request recovered in {rec_ms:.1f} ms")
+        f"({100 * out['hbm_frac']:.1f}% of HBM); one damaged request recovered in {rec_ms:.1f} ms, "
+        f"from its damaged block in {from_ms:.1f} ms")
+    return out
+
+
+def shared_prefix(wl, model, arena, ws, nbytes, kvr, S, steps, stream, log):
+    """Requests that all begin with the same S tokens (S a multiple of the
+    block size): request 0 computes them, the others list its first S/B
+    blocks read-only and start at S, all in one call (kv_rebuild_from).
+    Timed with HIP events like the main rebuild; covered positions are all
+    of every request's."""
+    import numpy as np
+    import torch
+    R, B = wl.num_requests, wl.block_size
+    offs = wl.request_offsets()
+    head = wl.tokens[offs[0]:offs[0] + S]
+    if S % B or any(wl.lens[r] < S or not np.array_equal(wl.tokens[offs[r]:offs[r] + S], head)
+                    for r in range(R)):
+        raise SystemExit(f"--shared-prefix {S}: the requests do not all begin with the same {S} tokens "
+                         f"(or {S} is not a multiple of the block size {B})")
+    tables = wl.block_tables.copy()
+    tables[1:, :S // B] = tables[0, :S // B]
+    starts = np.array([0] + [S] * (R - 1), np.int32)
+    toks = np.concatenate([wl.tokens[offs[r] + starts[r]:offs[r] + wl.lens[r]] for r in range(R)])
+    plan = kvr.kv_rebuild_stage_from(arena.handle, toks, wl.lens, starts, tables, ws.data_ptr(), nbytes,
+                                     stream)
+    kvr.kv_rebuild_execute(model.weights, plan, stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        kvr.kv_rebuild_execute(model.weights, plan, stream)
+    e1.record()
+    torch.cuda.synchronize()
+    kvr.kv_plan_release(plan)
+    ms = e0.elapsed_time(e1) / steps
+    covered, computed = int(wl.lens.sum()), int(len(toks))
+    out = {"shared_tokens": S, "requests": R, "positions_covered": covered,
+           "positions_computed": computed, "ms_per_step": ms,
+           "covered_tokens_per_s": covered / (ms / 1e3)}
+    log(f"[bench] shared prefix of {S}: {computed} of {covered} positions computed, {ms:.1f} ms per "
+        f"step, {out['covered_tokens_per_s']:.0f} covered tokens/s")
     return out
 
 
@@ -256,6 +322,8 @@ def main():
     ap.add_argument("--no-check", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=4,
                     help="resumed-decode steps timed after the rebuild (0 = none)")
+    ap.add_argument("--shared-prefix", type=int, default=0,
+                    help="also time a rebuild whose requests share their first N tokens' blocks")
     ap.add_argument("--verify-reps", type=int, default=20,
                     help="timed block-digest verification scans after the rebuild (0 = skip)")
     ap.add_argument("--copy-probe", type=int, default=0,
@@ -375,6 +443,11 @@ def main():
     if args.decode_steps > 0 and wl.num_requests > 0:
         dec = resume_decode(wl, model, arena, Hn, kvr, W, args.decode_steps, stream, log)
 
+    sp = None
+    if args.shared_prefix > 0:
+        sp = shared_prefix(wl, model, arena, ws, nbytes, kvr, args.shared_prefix, max(1, args.steps), stream,
+                           log)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
@@ -412,6 +485,7 @@ def main():
         "arena_check": check,
         "resume_decode": dec,
         "flush_free": ff,
+        "shared_prefix": sp,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
