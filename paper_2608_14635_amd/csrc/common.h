@@ -61,7 +61,10 @@ __device__ __forceinline__ void ld8(const float* p, float* v) {
   v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
-__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+// silu(g) = g * sigmoid(g); the reciprocal is v_rcp_f32 (1 ulp), far below
+// the bf16 rounding the SwiGLU output gets.  g very negative: exp overflows
+// to +inf and the result is -0, the limit.
+__device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
 // Wave-wide reductions (64 lanes).
 __device__ __forceinline__ float wave_sum(float v) {

@@ -214,6 +214,7 @@ __device__ __forceinline__ void epi_swiglu(const float* sC, int ldc, int rows, i
   const int tid = threadIdx.x;
   constexpr int HB = BN / 2;
   const int per_row = HB / 8;
+#pragma unroll 4
   for (int it = tid; it < rows * per_row; it += NT) {
     const int r = it / per_row, c0 = (it % per_row) * 8;
     const int m = m_base + r;
