@@ -180,14 +180,17 @@ __device__ __forceinline__ void epi_resid(const float* sC, int ldc, int rows, in
     const int r = it / per_row, c0 = (it % per_row) * 4;
     const int m = m_base + r;
     if (m >= M) continue;
-    float4* xp = reinterpret_cast<float4*>(e.x + (int64_t)m * e.ldx + n0 + c0);
+    // X is read and written once per product: nontemporal, so that it does
+    // not evict the operand panels other tiles are streaming through L2
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    f32x4* xp = reinterpret_cast<f32x4*>(e.x + (int64_t)m * e.ldx + n0 + c0);
     const float* src = sC + (int64_t)r * ldc + c0;
-    float4 xv = *xp;
+    f32x4 xv = __builtin_nontemporal_load(xp);
     xv.x += src[0];
     xv.y += src[1];
     xv.z += src[2];
     xv.w += src[3];
-    *xp = xv;
+    __builtin_nontemporal_store(xv, xp);
   }
 }
 
