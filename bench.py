@@ -299,8 +299,18 @@ def cpu_baseline(wl, model, Hn):
     c = (time.perf_counter() - tk0) / nk
     n = wl.lens.astype(np.float64)
     t_pred = float(np.sum((s.num_layers - 1) * (a * n + b * n * n) + c * n))
+    # check of the model: a complete oracle run of all layers over one short
+    # request (layer 0's weights in every layer: the time depends only on the
+    # shapes), sized to ~5 s, against the fitted per-layer time
+    L = s.num_layers
+    nm = int(min(n1, max(8, 5.0 / (L * a) // 8 * 8)))
+    tm = o.time_layers(s, {"embed": host["embed"], "layers": [host["layer0"]] * L},
+                       rng.integers(0, s.vocab, nm), L)
+    tm_pred = L * (a * nm + b * nm * nm)
     return {"value": wl.total_tokens / t_pred, "unit": "tokens/s", "cores": o.num_threads(),
             "kind": "oracle",
+            "model_check": {"tokens": nm, "layers": L, "measured_s": tm, "predicted_s": tm_pred,
+                            "ratio": tm / tm_pred},
             "sample": (f"oracle timed on one layer of the same shape at n={n1} ({t1:.1f}s) and "
                        f"n={n2} ({t2:.1f}s) plus layer-0 K/V rows of {nk} tokens ({c * nk:.2f}s); "
                        f"fitted t_layer(n)=a*n+b*n^2 extrapolated to {s.num_layers} layers x "

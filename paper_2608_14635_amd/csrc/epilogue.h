@@ -171,20 +171,47 @@ __device__ __forceinline__ void epi_qkv(float* sC, int ldc, int rows, int m_base
   }
 }
 
+// RESID: X += acc on the fp32 residual stream, read and written nontemporally
+// (once per product; it should not evict the operand panels other tiles are
+// streaming through L2).  Loads and stores share one wait counter on this
+// GPU, and once a store is pending every wait for a load becomes a wait for
+// all: so a batch of rows is loaded, summed and only then stored, with no
+// store between a load and its use.  A thread keeps one 4-column chunk; rows
+// are NT/(BN/4) apart.  Tiles cut by M take the plain row-by-row loop.
 template <int BN, int NT>
 __device__ __forceinline__ void epi_resid(const float* sC, int ldc, int rows, int m_base, int M,
                                           int n0, const EpiParams& e) {
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  constexpr int PER_ROW = BN / 4, RSTEP = NT / PER_ROW, RB = 16;
   const int tid = threadIdx.x;
-  const int per_row = BN / 4;
-  for (int it = tid; it < rows * per_row; it += NT) {
-    const int r = it / per_row, c0 = (it % per_row) * 4;
+  const int c0 = (tid % PER_ROW) * 4, r0 = tid / PER_ROW;
+  if (m_base + rows <= M && rows % (RSTEP * RB) == 0) {
+    for (int rb = 0; rb < rows; rb += RSTEP * RB) {
+      f32x4* xp = reinterpret_cast<f32x4*>(e.x + (int64_t)(m_base + rb + r0) * e.ldx + n0 + c0);
+      const int64_t step = (int64_t)RSTEP * e.ldx / 4;  // f32x4 units between this thread's rows
+      f32x4 xv[RB];
+#pragma unroll
+      for (int b = 0; b < RB; ++b) xv[b] = __builtin_nontemporal_load(xp + b * step);
+#pragma unroll
+      for (int b = 0; b < RB; ++b) {
+        const float* src = sC + (int64_t)(rb + r0 + b * RSTEP) * ldc + c0;
+        xv[b].x += src[0];
+        xv[b].y += src[1];
+        xv[b].z += src[2];
+        xv[b].w += src[3];
+        asm volatile("" : "+v"(xv[b]));  // the sum is formed here, before any store
+      }
+#pragma unroll
+      for (int b = 0; b < RB; ++b) __builtin_nontemporal_store(xv[b], xp + b * step);
+    }
+    return;
+  }
+  for (int it = tid; it < rows * PER_ROW; it += NT) {
+    const int r = it / PER_ROW, c = (it % PER_ROW) * 4;
     const int m = m_base + r;
     if (m >= M) continue;
-    // X is read and written once per product: nontemporal, so that it does
-    // not evict the operand panels other tiles are streaming through L2
-    typedef float f32x4 __attribute__((ext_vector_type(4)));
-    f32x4* xp = reinterpret_cast<f32x4*>(e.x + (int64_t)m * e.ldx + n0 + c0);
-    const float* src = sC + (int64_t)r * ldc + c0;
+    f32x4* xp = reinterpret_cast<f32x4*>(e.x + (int64_t)m * e.ldx + n0 + c);
+    const float* src = sC + (int64_t)r * ldc + c;
     f32x4 xv = __builtin_nontemporal_load(xp);
     xv.x += src[0];
     xv.y += src[1];
