@@ -480,12 +480,15 @@ void launch_rope_rows(float2* table, const int32_t* positions, int rows, int d, 
 }
 
 int decode_attn_splits(int num_requests, int nkv, int64_t max_ctx) {
-  // about 8192 (request, kv head, key range) items in all, at least 64 keys
-  // and at most 128 ranges per (request, kv head); never more for more
-  // requests, so a workspace sized for one request's split count fits any
-  // larger batch
+  // enough (request, kv head, key range) items to keep HBM busy (about 2048)
+  // and ranges of at most about 2048 keys, so the longest request's waves
+  // do not trail the rest (measured: 16 requests x 128K context and 64 x
+  // 1.2M both run best at 16 ranges; shorter ranges spend their time on each
+  // wave's fixed costs); at least 64 keys and at most 128 ranges per
+  // (request, kv head).  Never more for more requests, so a workspace sized
+  // for one request's split count fits any larger batch.
   const int64_t pairs = std::max<int64_t>(1, (int64_t)num_requests * nkv);
-  const int64_t want = (8192 + pairs - 1) / pairs;
+  const int64_t want = std::max<int64_t>((2048 + pairs - 1) / pairs, (max_ctx + 2047) / 2048);
   const int64_t cap = std::min<int64_t>(DMAXS, (max_ctx + 63) / 64);
   return (int)std::max<int64_t>(1, std::min(want, cap));
 }
