@@ -16,6 +16,141 @@
 
 namespace kvr {
 
+// Full-tile fast paths of the QKV epilogue for head dim 128 without bias
+// or per-head norm (every row of the tile below M).  Loads and stores share
+// one wait counter on this GPU: once a store is pending, waiting for a load
+// means waiting for everything, so each batch of rows loads all it needs
+// (positions, slots, key rows, then the RoPE rows), forms every result and
+// only then stores.  A thread keeps one (head, chunk of 8 rotary pairs).
+template <typename T, int BN, int NT, int REGION>
+__device__ __forceinline__ void epi_qkv_rot_full(const float* sC, int ldc, int rows, int m_base, int n0,
+                                                 const EpiParams& e) {
+  constexpr int D = 128, HALF = 64, CH = HALF / 8, PER_ROW = (BN / D) * CH, RSTEP = NT / PER_ROW, RB = 4;
+  const int tid = threadIdx.x;
+  const int hc = tid % PER_ROW, hh = hc / CH, c0 = (hc % CH) * 8;
+  const int qcols = e.nq * D;
+  const int kh = REGION == 1 ? (n0 - qcols) / D + hh : 0;
+  // a missing key-row map reads the positions instead (valid memory) and
+  // the value is replaced by the row
+  const bool has_krow = e.krow != nullptr;
+  const int32_t* krow = has_krow ? e.krow : e.pos;
+  for (int rb = tid / PER_ROW; rb < rows; rb += RSTEP * RB) {
+    int pos[RB];
+    int64_t sl[RB], kr[RB];
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      const int m = m_base + rb + b * RSTEP;
+      pos[b] = e.pos[m];
+      if (REGION == 1) {
+        sl[b] = e.slot[m];
+        const int k = krow[m];
+        kr[b] = has_krow ? k : m;
+      }
+    }
+    float2 cs[RB][8];
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      const float4* src = reinterpret_cast<const float4*>(e.rope + (int64_t)pos[b] * HALF + c0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float4 v = src[i];
+        cs[b][2 * i] = make_float2(v.x, v.y);
+        cs[b][2 * i + 1] = make_float2(v.z, v.w);
+      }
+    }
+    float lo[RB][8], hi[RB][8];
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      const float* src = sC + (int64_t)(rb + b * RSTEP) * ldc + hh * D;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float a = src[c0 + i], bv = src[c0 + HALF + i];
+        const float2 t = cs[b][i];
+        lo[b][i] = Elem<T>::round(a * t.x - bv * t.y);
+        hi[b][i] = Elem<T>::round(bv * t.x + a * t.y);
+        // padding rows: zeros in the K copy (keys past a request's end are
+        // inert), nothing in the arena
+        if (REGION == 1 && sl[b] < 0) lo[b][i] = hi[b][i] = 0.0f;
+        asm volatile("" : "+v"(lo[b][i]), "+v"(hi[b][i]));
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      const int64_t m = m_base + rb + b * RSTEP;
+      if (REGION == 0) {
+        T* dst = reinterpret_cast<T*>(e.q_out) + m * qcols + n0 + hh * D;
+        store8(dst + c0, lo[b]);
+        store8(dst + c0 + HALF, hi[b]);
+      } else {
+        if (e.kc != nullptr) {
+          T* kd = reinterpret_cast<T*>(e.kc) + ((int64_t)kh * e.ldvt + kr[b]) * D;
+          store8(kd + c0, lo[b]);
+          store8(kd + c0 + HALF, hi[b]);
+        }
+        if (sl[b] >= 0) {
+          T* dst = reinterpret_cast<T*>(e.arena_k) + (sl[b] * e.nkv + kh) * (int64_t)D;
+          store8(dst + c0, lo[b]);
+          store8(dst + c0 + HALF, hi[b]);
+        }
+      }
+    }
+  }
+}
+
+// V columns of a full tile without bias: arena rows (slots loaded a batch at
+// a time before the stores), each row's padding flag and key row parked in
+// the tile's spare columns BN, BN+1, then the V^T columns from LDS only.
+template <typename T, int BN, int NT>
+__device__ __forceinline__ void epi_qkv_v_full(float* sC, int ldc, int rows, int m_base, int n0,
+                                               const EpiParams& e) {
+  constexpr int PER_ROW = BN / 8, RSTEP = NT / PER_ROW, RB = 8;
+  const int tid = threadIdx.x;
+  const int c0 = (tid % PER_ROW) * 8;
+  const int kcols = e.nkv * e.d, vbase = n0 - e.nq * e.d - kcols;
+  const bool has_krow = e.krow != nullptr;
+  const int32_t* krow = has_krow ? e.krow : e.pos;
+  for (int rb = tid / PER_ROW; rb < rows; rb += RSTEP * RB) {
+    int64_t sl[RB];
+    int kr[RB];
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      const int m = m_base + rb + b * RSTEP;
+      sl[b] = e.slot[m];
+      const int k = krow[m];
+      kr[b] = has_krow ? k : m;
+      asm volatile("" : "+v"(sl[b]), "+v"(kr[b]));
+    }
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      const int r = rb + b * RSTEP;
+      float* row = sC + (int64_t)r * ldc;
+      if (c0 == 0) {
+        row[BN] = sl[b] < 0 ? 1.0f : 0.0f;
+        row[BN + 1] = __int_as_float(kr[b]);
+      }
+      if (sl[b] < 0) continue;  // padding row
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = row[c0 + i];
+      store8(reinterpret_cast<T*>(e.arena_v) + sl[b] * (int64_t)kcols + vbase + c0, v);
+    }
+  }
+  if (e.vt == nullptr) return;
+  __syncthreads();
+  // V^T[col][krow(m)]: 8 consecutive rows of one column per item (their key
+  // rows are consecutive: a request's rows start on a multiple of 8, and so
+  // do its suffix key rows); padding rows get zeros
+  for (int it = tid; it < BN * (rows / 8); it += NT) {
+    const int c = it % BN, rc = it / BN;
+    const float* src = sC + (int64_t)(rc * 8) * ldc;
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = src[(int64_t)i * ldc + BN] != 0.0f ? 0.0f : src[(int64_t)i * ldc + c];
+    const int64_t kr0 = __float_as_int(src[BN + 1]);
+    store8(reinterpret_cast<T*>(e.vt) + (int64_t)(vbase + c) * e.ldvt + kr0, v);
+  }
+}
+
 // QKV: the tile covers logical columns [n0, n0+BN) lying in one region
 // (q: [0, nq*d), k: [nq*d, nq*d + nkv*d), v: after that) and BN % d == 0.
 // Variants: biases are added to the accumulators first; with per-head q/k
@@ -29,6 +164,21 @@ __device__ __forceinline__ void epi_qkv(float* sC, int ldc, int rows, int m_base
   const int d = e.d, half = d >> 1;
   const int qcols = e.nq * d, kcols = e.nkv * d;
   const int region = n0 < qcols ? 0 : (n0 < qcols + kcols ? 1 : 2);
+  if (d == 128 && m_base + rows <= M && BN % 128 == 0 && NT % ((BN / 128) * 8) == 0 &&
+      rows % (NT / ((BN / 128) * 8) * 4) == 0 && ldc >= BN + 2) {
+    if (region == 0 && e.bq == nullptr && e.q_norm == nullptr) {
+      epi_qkv_rot_full<T, BN, NT, 0>(sC, ldc, rows, m_base, n0, e);
+      return;
+    }
+    if (region == 1 && e.bk == nullptr && e.k_norm == nullptr) {
+      epi_qkv_rot_full<T, BN, NT, 1>(sC, ldc, rows, m_base, n0, e);
+      return;
+    }
+    if (region == 2 && e.bv == nullptr && NT % (BN / 8) == 0 && rows % (NT / (BN / 8) * 8) == 0) {
+      epi_qkv_v_full<T, BN, NT>(sC, ldc, rows, m_base, n0, e);
+      return;
+    }
+  }
   if (region < 2) {
     // column base of the tile within its region (q: head-major q columns,
     // k: head-major k columns), bias and norm gain of the region
