@@ -16,8 +16,8 @@
 
 namespace kvr {
 
-// Full-tile fast paths of the QKV epilogue for head dim 128 without bias
-// or per-head norm (every row of the tile below M).  Loads and stores share
+// Full-tile fast paths of the QKV epilogue for head dim 128 (every row of
+// the tile below M).  Loads and stores share
 // one wait counter on this GPU: once a store is pending, waiting for a load
 // means waiting for everything, so each batch of rows loads all it needs
 // (positions, slots, key rows, then the RoPE rows), forms every result and
@@ -30,6 +30,22 @@ __device__ __forceinline__ void epi_qkv_rot_full(const float* sC, int ldc, int r
   const int hc = tid % PER_ROW, hh = hc / CH, c0 = (hc % CH) * 8;
   const int qcols = e.nq * D;
   const int kh = REGION == 1 ? (n0 - qcols) / D + hh : 0;
+  // bias and per-head norm gain of this thread's columns (fixed per thread);
+  // the norm's inverse RMS per (row, head) sits in column BN + hh
+  const T* bias = reinterpret_cast<const T*>(REGION == 0 ? e.bq : e.bk);
+  const T* gain = reinterpret_cast<const T*>(REGION == 0 ? e.q_norm : e.k_norm);
+  const int hb = (REGION == 0 ? n0 : n0 - qcols) + hh * D;
+  float ba[8], bb[8], ga[8], gb[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ba[i] = bb[i] = 0.0f, ga[i] = gb[i] = 1.0f;
+  if (bias != nullptr) {
+    ld8(bias + hb + c0, ba);
+    ld8(bias + hb + c0 + HALF, bb);
+  }
+  if (gain != nullptr) {
+    ld8(gain + c0, ga);
+    ld8(gain + c0 + HALF, gb);
+  }
   // a missing key-row map reads the positions instead (valid memory) and
   // the value is replaced by the row
   const bool has_krow = e.krow != nullptr;
@@ -62,9 +78,18 @@ __device__ __forceinline__ void epi_qkv_rot_full(const float* sC, int ldc, int r
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
       const float* src = sC + (int64_t)(rb + b * RSTEP) * ldc + hh * D;
+      const float inv = gain != nullptr ? sC[(int64_t)(rb + b * RSTEP) * ldc + BN + hh] : 1.0f;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const float a = src[c0 + i], bv = src[c0 + HALF + i];
+        float a = src[c0 + i], bv = src[c0 + HALF + i];
+        if (bias != nullptr) {
+          a += ba[i];
+          bv += bb[i];
+        }
+        if (gain != nullptr) {
+          a = a * inv * ga[i];
+          bv = bv * inv * gb[i];
+        }
         const float2 t = cs[b][i];
         lo[b][i] = Elem<T>::round(a * t.x - bv * t.y);
         hi[b][i] = Elem<T>::round(bv * t.x + a * t.y);
@@ -164,20 +189,20 @@ __device__ __forceinline__ void epi_qkv(float* sC, int ldc, int rows, int m_base
   const int d = e.d, half = d >> 1;
   const int qcols = e.nq * d, kcols = e.nkv * d;
   const int region = n0 < qcols ? 0 : (n0 < qcols + kcols ? 1 : 2);
-  if (d == 128 && m_base + rows <= M && BN % 128 == 0 && NT % ((BN / 128) * 8) == 0 &&
-      rows % (NT / ((BN / 128) * 8) * 4) == 0 && ldc >= BN + 2) {
-    if (region == 0 && e.bq == nullptr && e.q_norm == nullptr) {
-      epi_qkv_rot_full<T, BN, NT, 0>(sC, ldc, rows, m_base, n0, e);
-      return;
+  const bool full = d == 128 && m_base + rows <= M && BN % 128 == 0 && NT % ((BN / 128) * 8) == 0 &&
+                    rows % (NT / ((BN / 128) * 8) * 4) == 0 && ldc >= BN + 2;
+  if (full && region == 2 && NT % (BN / 8) == 0 && rows % (NT / (BN / 8) * 8) == 0) {
+    const T* bias = reinterpret_cast<const T*>(e.bv);
+    if (bias != nullptr) {
+      // fold the bias into the parked tile once; both stores read it
+      for (int it = tid; it < rows * BN; it += NT) {
+        const int r = it / BN, c = it % BN;
+        sC[(int64_t)r * ldc + c] += Elem<T>::load(bias, (n0 - qcols - kcols) + c);
+      }
+      __syncthreads();
     }
-    if (region == 1 && e.bk == nullptr && e.k_norm == nullptr) {
-      epi_qkv_rot_full<T, BN, NT, 1>(sC, ldc, rows, m_base, n0, e);
-      return;
-    }
-    if (region == 2 && e.bv == nullptr && NT % (BN / 8) == 0 && rows % (NT / (BN / 8) * 8) == 0) {
-      epi_qkv_v_full<T, BN, NT>(sC, ldc, rows, m_base, n0, e);
-      return;
-    }
+    epi_qkv_v_full<T, BN, NT>(sC, ldc, rows, m_base, n0, e);
+    return;
   }
   if (region < 2) {
     // column base of the tile within its region (q: head-major q columns,
@@ -213,6 +238,13 @@ __device__ __forceinline__ void epi_qkv(float* sC, int ldc, int rows, int m_base
         if (part == 0) sC[(int64_t)r * ldc + BN + hh] = 1.0f / sqrtf(ss / (float)d + e.eps);
       }
       __syncthreads();
+    }
+    if (full) {
+      if (region == 0)
+        epi_qkv_rot_full<T, BN, NT, 0>(sC, ldc, rows, m_base, n0, e);
+      else
+        epi_qkv_rot_full<T, BN, NT, 1>(sC, ldc, rows, m_base, n0, e);
+      return;
     }
     // items: (row, head in tile, chunk of 8 rotary pairs)
     const int per_row = heads * chunks;
