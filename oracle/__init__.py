@@ -35,7 +35,8 @@ class _Model(C.Structure):
     _fields_ = [("num_layers", C.c_int32), ("hidden", C.c_int32), ("num_q_heads", C.c_int32),
                 ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn_dim", C.c_int32),
                 ("vocab", C.c_int32), ("rms_eps", C.c_double), ("rope_theta", C.c_double),
-                ("dtype", C.c_int32), ("qk_norm", C.c_int32), ("qkv_bias", C.c_int32)]
+                ("dtype", C.c_int32), ("qk_norm", C.c_int32), ("qkv_bias", C.c_int32),
+                ("round_p", C.c_int32)]
 
 
 _LAYER_KEYS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down",
@@ -95,12 +96,14 @@ class Oracle:
 
     # -- marshalling -------------------------------------------------
     @staticmethod
-    def _model(shape, dtype: Optional[int] = None, num_layers: Optional[int] = None) -> _Model:
+    def _model(shape, dtype: Optional[int] = None, num_layers: Optional[int] = None,
+               round_p: bool = False) -> _Model:
         return _Model(num_layers if num_layers is not None else shape.num_layers, shape.hidden,
                       shape.num_q_heads, shape.num_kv_heads, shape.head_dim, shape.ffn_dim,
                       shape.vocab, float(shape.rms_eps), float(shape.rope_theta),
                       shape.dtype if dtype is None else dtype,
-                      int(getattr(shape, "qk_norm", False)), int(getattr(shape, "qkv_bias", False)))
+                      int(getattr(shape, "qk_norm", False)), int(getattr(shape, "qkv_bias", False)),
+                      int(round_p))
 
     @staticmethod
     def _check(a: np.ndarray, dt: int) -> np.ndarray:
@@ -123,11 +126,12 @@ class Oracle:
     # -- calls --------------------------------------------------------
     def rebuild(self, shape, weights: Dict, tokens, lens, tables, arena: np.ndarray,
                 block_size: int, num_blocks: int, mode: str = "prefill",
-                dtype: Optional[int] = None, final_hidden: bool = False):
+                dtype: Optional[int] = None, final_hidden: bool = False, round_p: bool = False):
         """Run the oracle in place on `arena` (raw host array of the dtype).
-        Returns the final fp64 hidden state [T, H] when final_hidden is set."""
+        Returns the final fp64 hidden state [T, H] when final_hidden is set.
+        round_p: attention weights rounded to the dtype before P.V (kvo.h)."""
         dt = shape.dtype if dtype is None else dtype
-        m = self._model(shape, dt)
+        m = self._model(shape, dt, round_p=round_p)
         tokens, lens = self._i32(tokens), self._i32(lens)
         tables = self._i32(tables)
         max_blocks = tables.shape[1] if tables.ndim == 2 else 0

@@ -26,6 +26,12 @@
  * Every reduction is a plain sequential fp64 sum; every op output is rounded
  * to fp32 before the next op; rnd() is the identity for fp32 models and
  * fp32 -> bf16 round-to-nearest-even for bf16 models.  KVO_F64 rounds nothing.
+ *
+ * Optional mode round_p: the attention weights w_j = exp(z_j - max z) are
+ * rounded like an op output (rnd(fp32(w_j))) before both the weighted sum of
+ * V^ and the denominator.  It models a freedom the GPU path declares (its
+ * P.V product takes P in the model dtype); the definition above is the mode
+ * off.
  */
 #include "kvo.h"
 
@@ -253,6 +259,7 @@ static void layer_step(const kvo_model* m, const kvo_layer* lw, int l, double* x
     }
     for (j = 0; j <= p; ++j) {
       z[j] = exp(z[j] - zmax);
+      if (m->round_p) z[j] = rnd(to_work(z[j], dt), dt);
       den += z[j];
     }
     for (e = 0; e < d; ++e) {

@@ -41,6 +41,9 @@ typedef struct {
   int32_t dtype;         /* element type of weights and arena: KVO_F32/BF16/F64 */
   int32_t qk_norm;       /* 1: per-head RMSNorm of q and k before RoPE (Qwen3)   */
   int32_t qkv_bias;      /* 1: q, k, v projections carry a bias (Qwen2.5)        */
+  int32_t round_p;       /* 1: attention weights P = exp(z - max z) rounded to the
+                            model dtype before the P.V sum and the denominator
+                            (the GPU's declared freedom; 0 = the definition)   */
 } kvo_model;
 
 /* One layer's weights, host pointers, nn.Linear layout [out, in] row-major.

@@ -71,11 +71,11 @@ def weights_in(w: dict, src_dt: int, dst_dt: int) -> dict:
     return {"embed": cv(f["embed"]), "layers": [{k: cv(v) for k, v in lw.items()} for lw in f["layers"]]}
 
 
-def run(o, shape, w, wl, dt=None, mode="prefill", arena=None, final_hidden=False):
+def run(o, shape, w, wl, dt=None, mode="prefill", arena=None, final_hidden=False, round_p=False):
     dt = shape.dtype if dt is None else dt
     a = W.host_arena(wl, dt) if arena is None else arena
     fh = o.rebuild(shape, w, wl.tokens, wl.lens, wl.block_tables, a, wl.block_size,
-                   wl.num_blocks, mode=mode, dtype=dt, final_hidden=final_hidden)
+                   wl.num_blocks, mode=mode, dtype=dt, final_hidden=final_hidden, round_p=round_p)
     return (a, fh) if final_hidden else a
 
 
@@ -279,11 +279,11 @@ def pin_gqa_equals_mha(o):
             assert np.array_equal(vm[:, :, h], v[:, :, h // g]), "GQA V != MHA V"
 
 
-def _torch_compare(o, shape, wl, w, dt, rounding, tol, min_exact=None):
+def _torch_compare(o, shape, wl, w, dt, rounding, tol, min_exact=None, round_p=False):
     import torch_ref
-    a = run(o, shape, w, wl, dt=dt)
+    a = run(o, shape, w, wl, dt=dt, round_p=round_p)
     w64 = torch_ref.weights_f64(w, dt)
-    refs = torch_ref.forward_batch(shape, w64, wl, rounding)
+    refs = torch_ref.forward_batch(shape, w64, wl, rounding, round_p)
     worst, exact, total = 0.0, 0, 0
     for r in range(wl.num_requests):
         if refs[r] is None:
@@ -327,6 +327,18 @@ def pin_torch_bf16_rounding(o):
     wl = W.small_workload(shape, [1, 17, 70], seed=71)
     w = W.host_weights(shape, seed=17)
     _torch_compare(o, shape, wl, w, BF16, "bf16", 1e-3, min_exact=0.999)
+
+
+def pin_torch_bf16_rounding_round_p(o):
+    """round_p mode against the same torch forward with the attention written
+    out and its weights rounded before P.V and the denominator; the mode
+    must change the result (P rounding is not a no-op)."""
+    shape = TINY_BF16_2L
+    wl = W.small_workload(shape, [1, 17, 70], seed=71)
+    w = W.host_weights(shape, seed=17)
+    _torch_compare(o, shape, wl, w, BF16, "bf16", 1e-3, min_exact=0.999, round_p=True)
+    plain, rp = run(o, shape, w, wl), run(o, shape, w, wl, round_p=True)
+    assert not np.array_equal(plain, rp), "round_p left the bf16 rebuild unchanged"
 
 
 def pin_bf16_rounding_matches_torch(o):

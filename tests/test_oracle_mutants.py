@@ -69,6 +69,10 @@ MUTANTS = [
      "if (dg == committed[e]) intact[r] += 1;", 0),
     ("verify_tail_block_full", "const int32_t n = lens[r] - j * B < B ? lens[r] - j * B : B;",
      "const int32_t n = B;", 0),
+    ("round_p_ignored", "if (m->round_p) z[j] = rnd(to_work(z[j], dt), dt);", "", 0),
+    ("round_p_denominator_unrounded",
+     "      if (m->round_p) z[j] = rnd(to_work(z[j], dt), dt);\n      den += z[j];",
+     "      den += z[j];\n      if (m->round_p) z[j] = rnd(to_work(z[j], dt), dt);", 0),
 ]
 
 

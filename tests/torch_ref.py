@@ -10,6 +10,8 @@ from __future__ import annotations
 
 from typing import Dict, List, Optional, Tuple
 
+import math
+
 import numpy as np
 import torch
 import torch.nn.functional as F
@@ -32,9 +34,12 @@ def _rotate_half(x: torch.Tensor) -> torch.Tensor:
 
 
 def forward(shape: W.ModelShape, w64: Dict, tokens: np.ndarray,
-            rounding: Optional[str] = None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+            rounding: Optional[str] = None, round_p: bool = False
+            ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
     """One request.  Returns K [L, n, nkv, d], V [L, n, nkv, d] (rounded as
-    stored) and the final residual [n, H]."""
+    stored) and the final residual [n, H].  round_p: attention written out
+    as softmax weights exp(z - max z), rounded like an op output, then
+    (P V) / sum(P), instead of scaled_dot_product_attention."""
     n = len(tokens)
     H, d, nq, nkv = shape.hidden, shape.head_dim, shape.num_q_heads, shape.num_kv_heads
 
@@ -73,9 +78,19 @@ def forward(shape: W.ModelShape, w64: Dict, tokens: np.ndarray,
         v = rnd(v)
         Ks.append(k)
         Vs.append(v)
-        o = F.scaled_dot_product_attention(q.transpose(0, 1)[None], k.transpose(0, 1)[None],
-                                           v.transpose(0, 1)[None], is_causal=True,
-                                           enable_gqa=True)
+        if round_p:
+            g = nq // nkv
+            qh = q.transpose(0, 1)                                   # [nq, n, d]
+            kh = k.transpose(0, 1).repeat_interleave(g, dim=0)       # [nq, n, d]
+            vh = v.transpose(0, 1).repeat_interleave(g, dim=0)
+            z = torch.matmul(qh, kh.transpose(1, 2).contiguous()) / math.sqrt(d)
+            z = z.masked_fill(torch.triu(torch.ones(n, n, dtype=torch.bool), 1), float("-inf"))
+            pw = rnd(work(torch.exp(z - z.amax(dim=-1, keepdim=True))))
+            o = (torch.matmul(pw, vh) / pw.sum(dim=-1, keepdim=True))[None]
+        else:
+            o = F.scaled_dot_product_attention(q.transpose(0, 1)[None], k.transpose(0, 1)[None],
+                                               v.transpose(0, 1)[None], is_causal=True,
+                                               enable_gqa=True)
         u = rnd(work(o[0].transpose(0, 1).reshape(n, nq * d)))
         x = work(x + work(F.linear(u, lw["wo"])))
         b = rnd(F.rms_norm(x, (H,), weight=lw["ffn_norm"], eps=float(shape.rms_eps)))
@@ -86,7 +101,7 @@ def forward(shape: W.ModelShape, w64: Dict, tokens: np.ndarray,
     return torch.stack(Ks), torch.stack(Vs), x
 
 
-def forward_batch(shape, w64, wl: W.Workload, rounding=None) -> List:
+def forward_batch(shape, w64, wl: W.Workload, rounding=None, round_p: bool = False) -> List:
     off = wl.request_offsets()
     out = []
     for r in range(wl.num_requests):
@@ -94,7 +109,7 @@ def forward_batch(shape, w64, wl: W.Workload, rounding=None) -> List:
         if len(toks) == 0:
             out.append(None)
             continue
-        out.append(forward(shape, w64, toks, rounding))
+        out.append(forward(shape, w64, toks, rounding, round_p))
     return out
 
 
