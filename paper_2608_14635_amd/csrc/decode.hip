@@ -425,47 +425,94 @@ __global__ __launch_bounds__(DMAXD) void decode_combine_kernel(DecodeAttnParams 
 }
 
 // Greedy tokens from the transposed logits [vocab][ld], in two passes.
-// Pass 1: workgroup c scans a contiguous chunk of vocabulary rows; thread t
-// follows request t (a row's requests are contiguous, so loads coalesce) and
-// keeps the largest value, the lowest index among equal ones; it also copies
-// the logits out when asked.  Pass 2 merges the chunks of each request in
-// chunk order.
+// (value, index) pairs merge by the larger value and, among equal values, the
+// lower index, so the result is the lowest index among equal maxima whatever
+// the merge order.
+__device__ __forceinline__ void argmax_merge(float& best, int& bi, float b, int i) {
+  if (i >= 0 && (bi < 0 || b > best || (b == best && i < bi))) {
+    best = b;
+    bi = i;
+  }
+}
+
+// Pass 1: workgroup c scans a contiguous chunk of vocabulary rows.  With R <=
+// 256 requests, the 256/R threads of request r (t % R == r) take rows t/R,
+// t/R + 256/R, ... of the chunk, loading 8 rows before comparing (and, when
+// asked, copying the logits out), then merge through LDS; larger batches
+// keep one thread per request.  Pass 2 merges the chunks of each request.
 __global__ __launch_bounds__(256) void argmax_partial_kernel(const float* logits_t, int64_t ld,
                                                              int vocab, int R, float2* partial,
                                                              float* logits_out) {
+  __shared__ float s_best[256];
+  __shared__ int s_idx[256];
   const int c = blockIdx.x;
   const int per = (vocab + ARGMAX_CHUNKS - 1) / ARGMAX_CHUNKS;
   const int v0 = c * per, v1 = min(vocab, v0 + per);
-  for (int r = threadIdx.x; r < R; r += 256) {
-    float best = -INFINITY;
-    int bi = -1;
-    for (int v = v0; v < v1; ++v) {
-      const float z = logits_t[(int64_t)v * ld + r];
-      if (logits_out) logits_out[(int64_t)r * vocab + v] = z;
-      if (bi < 0 || z > best) {
-        best = z;
-        bi = v;
+  if (R > 256) {
+    for (int r = threadIdx.x; r < R; r += 256) {
+      float best = -INFINITY;
+      int bi = -1;
+      for (int v = v0; v < v1; ++v) {
+        const float z = logits_t[(int64_t)v * ld + r];
+        if (logits_out) logits_out[(int64_t)r * vocab + v] = z;
+        argmax_merge(best, bi, z, v);
+      }
+      partial[(int64_t)c * R + r] = make_float2(best, __int_as_float(bi));
+    }
+    return;
+  }
+  const int tpr = 256 / R, t = threadIdx.x, r = t % R, k = t / R;
+  float best = -INFINITY;
+  int bi = -1;
+  if (k < tpr) {
+    for (int vb = v0 + k; vb < v1; vb += 8 * tpr) {
+      float z[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int v = vb + u * tpr;
+        z[u] = v < v1 ? logits_t[(int64_t)v * ld + r] : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int v = vb + u * tpr;
+        if (v < v1) argmax_merge(best, bi, z[u], v);
+      }
+      if (logits_out) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int v = vb + u * tpr;
+          if (v < v1) logits_out[(int64_t)r * vocab + v] = z[u];
+        }
       }
     }
+  }
+  s_best[t] = best;
+  s_idx[t] = bi;
+  __syncthreads();
+  if (t < R) {
+    for (int j = 1; j < tpr; ++j) argmax_merge(best, bi, s_best[j * R + r], s_idx[j * R + r]);
     partial[(int64_t)c * R + r] = make_float2(best, __int_as_float(bi));
   }
 }
 
+// Pass 2: one wave per request; lane l merges chunks l, l+64, ..., then the
+// wave merges its lanes.
 __global__ __launch_bounds__(64) void argmax_final_kernel(const float2* partial, int R,
                                                           int32_t* next_tokens) {
-  const int r = blockIdx.x;
-  if (threadIdx.x != 0) return;
+  const int r = blockIdx.x, t = threadIdx.x;
   float best = -INFINITY;
   int bi = -1;
-  for (int c = 0; c < ARGMAX_CHUNKS; ++c) {
+  for (int c = t; c < ARGMAX_CHUNKS; c += 64) {
     const float2 e = partial[(int64_t)c * R + r];
-    const int i = __float_as_int(e.y);
-    if (i >= 0 && (bi < 0 || e.x > best)) {
-      best = e.x;
-      bi = i;
-    }
+    argmax_merge(best, bi, e.x, __float_as_int(e.y));
   }
-  next_tokens[r] = bi < 0 ? 0 : bi;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ob = __shfl_xor(best, o, 64);
+    const int oi = __shfl_xor(bi, o, 64);
+    argmax_merge(best, bi, ob, oi);
+  }
+  if (t == 0) next_tokens[r] = bi < 0 ? 0 : bi;
 }
 
 }  // namespace
