@@ -399,27 +399,58 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
 // then the fused epilogue, in 32-row x 256-column pieces, exactly as the
 // one-pass GEMM would apply it.
 constexpr int SK_ROWS = 32;
+
+// Sums the ksplit partials of IPT float4 items (item i at src[i], splits
+// stride apart) in split order, with SPB splits of every item loaded before
+// any is added, so the loads of a thread overlap instead of waiting one by one.
+template <int IPT, int SPB>
+__device__ __forceinline__ void sum_splits(const float* const (&src)[IPT], const bool (&valid)[IPT],
+                                           int ksplit, int64_t stride, float4 (&a)[IPT]) {
+  for (int sp0 = 0; sp0 < ksplit; sp0 += SPB) {
+    float4 v[IPT][SPB];
+#pragma unroll
+    for (int i = 0; i < IPT; ++i)
+#pragma unroll
+      for (int j = 0; j < SPB; ++j)
+        if (valid[i] && sp0 + j < ksplit) v[i][j] = *reinterpret_cast<const float4*>(src[i] + (sp0 + j) * stride);
+#pragma unroll
+    for (int i = 0; i < IPT; ++i)
+#pragma unroll
+      for (int j = 0; j < SPB; ++j) {
+        if (!valid[i] || sp0 + j >= ksplit) continue;
+        if (sp0 + j == 0) {
+          a[i] = v[i][j];
+        } else {
+          a[i].x += v[i][j].x;
+          a[i].y += v[i][j].y;
+          a[i].z += v[i][j].z;
+          a[i].w += v[i][j].w;
+        }
+      }
+  }
+}
+
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_epi_kernel(GemmParams p, int tiles_n) {
   __shared__ __attribute__((aligned(16))) float sC[SK_ROWS * LDC];
   const int tile_n = blockIdx.x % tiles_n, m0 = (blockIdx.x / tiles_n) * SK_ROWS;
   const int tid = threadIdx.x;
-  for (int it = tid; it < SK_ROWS * (BN / 4); it += 256) {
-    const int r = it / (BN / 4), c = (it % (BN / 4)) * 4;
-    const int m = m0 + r;
-    float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if (m < p.M) {
-      const float* src = p.part + (int64_t)m * p.part_ld + tile_n * BN + c;
-      a = *reinterpret_cast<const float4*>(src);
-      for (int sp = 1; sp < p.ksplit; ++sp) {
-        const float4 v = *reinterpret_cast<const float4*>(src + sp * p.part_stride);
-        a.x += v.x;
-        a.y += v.y;
-        a.z += v.z;
-        a.w += v.w;
-      }
-    }
-    *reinterpret_cast<float4*>(sC + r * LDC + c) = a;
+  constexpr int IPT = SK_ROWS * (BN / 4) / 256;
+  const float* src[IPT];
+  bool valid[IPT];
+  float4 a[IPT];
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int it = tid + i * 256, r = it / (BN / 4), c = (it % (BN / 4)) * 4;
+    valid[i] = m0 + r < p.M;
+    src[i] = p.part + (int64_t)min(m0 + r, p.M - 1) * p.part_ld + tile_n * BN + c;
+    a[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  }
+  sum_splits<IPT, 4>(src, valid, p.ksplit, p.part_stride, a);
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int it = tid + i * 256, r = it / (BN / 4), c = (it % (BN / 4)) * 4;
+    *reinterpret_cast<float4*>(sC + r * LDC + c) = a[i];
   }
   __syncthreads();
   if (EPI == EPI_QKV) {
@@ -434,53 +465,65 @@ __global__ __launch_bounds__(256) void splitk_epi_kernel(GemmParams p, int tiles
 }
 
 // ---- products of few rows (resumed decode) ----
-// C[M <= 64, N] = A . B^T, weight-stationary: each wave owns 16 output columns
-// (16 weight rows) and one K range, streams those rows once with 16-byte
-// loads (per 128-k chunk a lane takes 64 contiguous bytes of its row) and
-// multiplies them with every row of A on v_mfma_f32_16x16x32_bf16 (16-row
-// tiles of A; rows past M are clamped and their results dropped).  No LDS
-// and no padding work: HBM-bound on the weights, while A stays in L2.  In a
-// chunk of 128 k, MFMA t takes the k values 32t+8q..+7 from lane group
-// q = lane/16 (the matrix core's own operand layout), so each load
-// instruction reads 64 contiguous bytes of each of 16 rows and the next one
-// the rest of those lines; the loads are plain (cached), as nontemporal ones
-// would fetch the lines again.  Output: the fp32
-// partial sums of the K range, in the split-K partial layout.
+// C[M <= 64, N] = A . B^T, weight-stationary: a wave owns NBW blocks of 16
+// output columns (16 weight rows each) and one K range.  It streams those rows
+// once with 16-byte loads (per 128-k chunk a lane takes 64 contiguous bytes of
+// its row) and multiplies them with every row of A on
+// v_mfma_f32_16x16x32_bf16 (16-row tiles of A; rows past M are clamped and
+// their results dropped).  The A fragments of a chunk are loaded once for all
+// NBW blocks: with one block per wave, the A loads (from L2) equal the weight
+// bytes and bound the kernel.  In a chunk of 128 k, MFMA t takes the k values
+// 32t+8q..+7 from lane group q = lane/16 (the matrix core's own operand
+// layout), so each load instruction reads 64 contiguous bytes of each of 16
+// rows and the next one the rest of those lines; the loads are plain (cached),
+// as nontemporal ones would fetch the lines again.  The waves of one K range
+// are consecutive, so a workgroup's waves read the same A lines.  No LDS and
+// no padding work: HBM-bound on the weights.  Output: the fp32 partial sums of
+// the K range, in the split-K partial layout.
 constexpr int SK_CHUNK = 128;   // k per chunk
-constexpr int SK_UNROLL = 4;    // chunks in flight per wave
+constexpr int SK_UNROLL = 2;    // chunks in flight per wave
 constexpr int SK_MAX_M = 64;
-// waves a launch aims for (K is split to get there): fewer, longer waves for
-// the narrow products, more for the wide ones (measured best on the 8B shapes)
-constexpr int SK_WAVES_NARROW = 2048, SK_WAVES_WIDE = 8192, SK_NARROW_BLOCKS = 512;
+// K is split into ranges for about SK_WAVES waves, at most 16 where the
+// epilogue is elementwise (it sums the splits of every output in parallel)
+// and 8 where it works on whole tiles, whose few workgroups read every split
+// (measured best on the 8B shapes with weights not in the last-level cache)
+constexpr int SK_WAVES = 2048, SK_MAX_SPLIT_ELEM = 16, SK_MAX_SPLIT_TILE = 8;
 
-template <int MT>
-__global__ __launch_bounds__(256) void gemm_bf16_skinny_kernel(GemmParams p, int nblocks, int kc_per) {
+template <int MT, int NBW>
+__global__ __launch_bounds__(256) void gemm_bf16_skinny_kernel(GemmParams p, int ngroups, int kc_per) {
   const int lane = threadIdx.x & 63;
   const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (item >= nblocks * p.ksplit) return;  // whole waves
-  const int nb = item / p.ksplit, split = item % p.ksplit;
-  const int tile_n = nb / (BN / 16), c0 = (nb % (BN / 16)) * 16;
+  if (item >= ngroups * p.ksplit) return;  // whole waves
+  const int grp = item % ngroups, split = item / ngroups;
   const int r16 = lane & 15, q = lane >> 4;
-  const bf16_t* brow = b_row_ptr(p, tile_n, c0 + r16) + 8 * q;
+  const bf16_t* brow[NBW];
+#pragma unroll
+  for (int b = 0; b < NBW; ++b) {
+    const int nb = grp * NBW + b;
+    brow[b] = b_row_ptr(p, nb / (BN / 16), (nb % (BN / 16)) * 16 + r16) + 8 * q;
+  }
   const bf16_t* arow[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
     arow[mt] = reinterpret_cast<const bf16_t*>(p.A) + (int64_t)min(mt * 16 + r16, p.M - 1) * p.lda + 8 * q;
   const int KC = p.K / SK_CHUNK;
   const int kc0 = split * kc_per, kc1 = min(KC, kc0 + kc_per);
-  f32x4 acc[MT];
+  f32x4 acc[NBW][MT];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-  // SK_UNROLL chunks of loads in flight, then their MFMAs (the K range of a
-  // wave is a few chunks; a double-buffered loop measured slower here)
+  for (int b = 0; b < NBW; ++b)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[b][mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  // SK_UNROLL chunks of loads in flight (weights first), then their MFMAs
   for (int kc = kc0; kc < kc1; kc += SK_UNROLL) {
-    bf16x8 bv[SK_UNROLL][4], av[SK_UNROLL][MT][4];
+    bf16x8 bv[SK_UNROLL][NBW][4], av[SK_UNROLL][MT][4];
 #pragma unroll
     for (int u = 0; u < SK_UNROLL; ++u) {
       if (kc + u < kc1) {
         const int ko = (kc + u) * SK_CHUNK;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) bv[u][t] = *reinterpret_cast<const bf16x8*>(brow + ko + 32 * t);
+        for (int b = 0; b < NBW; ++b)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) bv[u][b][t] = *reinterpret_cast<const bf16x8*>(brow[b] + ko + 32 * t);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -493,20 +536,26 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny_kernel(GemmParams p, int
 #pragma unroll
         for (int t = 0; t < 4; ++t)
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u][mt][t], bv[u][t], acc[mt], 0, 0, 0);
+          for (int b = 0; b < NBW; ++b)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+              acc[b][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u][mt][t], bv[u][b][t], acc[b][mt], 0, 0, 0);
       }
     }
   }
-  // a lane holds rows 4q .. 4q+3 of each 16-row tile, at column c0 + r16
-  float* out = p.part + split * p.part_stride + tile_n * BN + c0 + r16;
+  // a lane holds rows 4q .. 4q+3 of each 16-row tile, at column r16 of a block
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+  for (int b = 0; b < NBW; ++b) {
+    const int nb = grp * NBW + b;
+    float* out = p.part + split * p.part_stride + nb * 16 + r16;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int m = mt * 16 + 4 * q + j;
-      if (m < p.M) out[(int64_t)m * p.part_ld] = acc[mt][j];
-    }
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int m = mt * 16 + 4 * q + j;
+        if (m < p.M) out[(int64_t)m * p.part_ld] = acc[b][mt][j];
+      }
+  }
 }
 
 // Elementwise epilogues (residual add, store) of a split-K product: one
@@ -518,18 +567,15 @@ __global__ __launch_bounds__(256) void splitk_elem_kernel(GemmParams p) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= (int64_t)p.M * ld4) return;
   const int m = (int)(i / ld4), col = (int)(i % ld4) * 4;
-  const float* src = p.part + (int64_t)m * p.part_ld + col;
-  float4 a = *reinterpret_cast<const float4*>(src);
-  for (int sp = 1; sp < p.ksplit; ++sp) {
-    const float4 v = *reinterpret_cast<const float4*>(src + sp * p.part_stride);
-    a.x += v.x;
-    a.y += v.y;
-    a.z += v.z;
-    a.w += v.w;
-  }
   float4* xp = reinterpret_cast<float4*>(p.epi.x + (int64_t)m * p.epi.ldx + p.n_begin + col);
+  float4 xv = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  if (EPI == EPI_RESID) xv = *xp;
+  const float* src[1] = {p.part + (int64_t)m * p.part_ld + col};
+  const bool valid[1] = {true};
+  float4 acc[1];
+  sum_splits<1, 8>(src, valid, p.ksplit, p.part_stride, acc);
+  const float4 a = acc[0];
   if (EPI == EPI_RESID) {
-    float4 xv = *xp;
     xv.x += a.x;
     xv.y += a.y;
     xv.z += a.z;
@@ -541,17 +587,24 @@ __global__ __launch_bounds__(256) void splitk_elem_kernel(GemmParams p) {
 }
 
 struct SkinnyPlan {
-  int nblocks, ksplit, kc_per;
+  int nbw, ngroups, ksplit, kc_per;
 };
 
 bool skinny_ok(int M, int K) { return M > 0 && M <= SK_MAX_M && K % SK_CHUNK == 0; }
 
-SkinnyPlan skinny_plan(int tiles_n, int K) {
+// 16-row blocks per wave: as many as keep the A tiles and the blocks' loads
+// in registers (MT tiles of A cost as much as MT blocks)
+int skinny_nbw(int M) {
+  const int mt = (M + 15) / 16;
+  return mt == 1 ? 4 : mt == 2 ? 2 : 1;
+}
+
+SkinnyPlan skinny_plan(int M, int tiles_n, int K, int max_split) {
   SkinnyPlan sp;
-  sp.nblocks = tiles_n * (BN / 16);
+  sp.nbw = skinny_nbw(M);
+  sp.ngroups = tiles_n * (BN / 16) / sp.nbw;
   const int KC = K / SK_CHUNK;
-  const int waves = sp.nblocks <= SK_NARROW_BLOCKS ? SK_WAVES_NARROW : SK_WAVES_WIDE;
-  const int want = std::max(1, std::min(KC, (waves + sp.nblocks - 1) / std::max(1, sp.nblocks)));
+  const int want = std::max(1, std::min({KC, max_split, SK_WAVES / std::max(1, sp.ngroups)}));
   sp.kc_per = (KC + want - 1) / want;
   sp.ksplit = (KC + sp.kc_per - 1) / sp.kc_per;
   return sp;
@@ -582,7 +635,8 @@ int group_m_for(int tiles_n) { return tiles_n <= 16 ? 4 : 8; }
 }  // namespace
 
 int64_t gemm_bf16_splitk_part_elems(int M, int N, int K) {
-  if (skinny_ok(M, K)) return (int64_t)skinny_plan(N / BN, K).ksplit * M * (N / BN) * BN;
+  if (skinny_ok(M, K))  // the larger of the two caps: enough for either epilogue
+    return (int64_t)skinny_plan(M, N / BN, K, SK_MAX_SPLIT_ELEM).ksplit * M * (N / BN) * BN;
   const SplitPlan sp = split_plan(M, N / BN, K);
   return (int64_t)sp.ksplit * M * sp.tiles_n * BN;
 }
@@ -598,15 +652,16 @@ void launch_gemm_bf16_splitk(int epi, const GemmParams& p, float* part, int64_t 
   q.part = part;
   q.part_ld = (int)ld;
   q.part_stride = (int64_t)p.M * ld;
-  if (skinny_ok(p.M, p.K) && (int64_t)skinny_plan(tiles_n, p.K).ksplit * p.M * ld <= part_cap) {
-    const SkinnyPlan kp = skinny_plan(tiles_n, p.K);
+  const int max_split = epi == EPI_RESID || epi == EPI_STORE ? SK_MAX_SPLIT_ELEM : SK_MAX_SPLIT_TILE;
+  if (skinny_ok(p.M, p.K) && (int64_t)skinny_plan(p.M, tiles_n, p.K, max_split).ksplit * p.M * ld <= part_cap) {
+    const SkinnyPlan kp = skinny_plan(p.M, tiles_n, p.K, max_split);
     q.ksplit = kp.ksplit;
-    const dim3 grid((unsigned)((kp.nblocks * kp.ksplit + 3) / 4)), block(256);
+    const dim3 grid((unsigned)((kp.ngroups * kp.ksplit + 3) / 4)), block(256);
     switch ((p.M + 15) / 16) {
-      case 1: hipLaunchKernelGGL(gemm_bf16_skinny_kernel<1>, grid, block, 0, s, q, kp.nblocks, kp.kc_per); break;
-      case 2: hipLaunchKernelGGL(gemm_bf16_skinny_kernel<2>, grid, block, 0, s, q, kp.nblocks, kp.kc_per); break;
-      case 3: hipLaunchKernelGGL(gemm_bf16_skinny_kernel<3>, grid, block, 0, s, q, kp.nblocks, kp.kc_per); break;
-      default: hipLaunchKernelGGL(gemm_bf16_skinny_kernel<4>, grid, block, 0, s, q, kp.nblocks, kp.kc_per); break;
+      case 1: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<1, 4>), grid, block, 0, s, q, kp.ngroups, kp.kc_per); break;
+      case 2: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<2, 2>), grid, block, 0, s, q, kp.ngroups, kp.kc_per); break;
+      case 3: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<3, 1>), grid, block, 0, s, q, kp.ngroups, kp.kc_per); break;
+      default: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<4, 1>), grid, block, 0, s, q, kp.ngroups, kp.kc_per); break;
     }
   } else {
     const SplitPlan sp = split_plan(p.M, tiles_n, p.K);
