@@ -1270,8 +1270,29 @@ kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void
     gd.epi.ldx = H;
     gemm(EPI_RESID, gd, s);
   }
-  // final norm, LM head (transposed: vocab rows x padded request columns), argmax
+  // final norm, LM head, argmax.  bf16: the few-row product writes row-major
+  // logits (into the caller's buffer when one is given); otherwise, and where
+  // the vocabulary is not a multiple of its blocks, the transposed product
+  // (vocab rows x padded request columns)
   launch_rmsnorm(dt, X, final_norm, A, R, H, eps, s);
+  if (dt == KV_BF16) {
+    GemmParams gr{};
+    gr.A = A;
+    gr.lda = H;
+    gr.M = R;
+    gr.K = H;
+    gr.B0 = lm_head;
+    gr.bmap = BMAP_PLAIN;
+    gr.n_begin = 0;
+    gr.n_end = d.vocab;
+    float* out = logits ? logits : logit_t;
+    if (launch_gemm_bf16_rows(gr, out, d.vocab, s)) {
+      launch_argmax_rows(out, d.vocab, d.vocab, R, amax, next_tokens, s);
+      const hipError_t err = hipGetLastError();
+      if (err != hipSuccess) return fail(KV_EDEVICE, "kernel launch failed: %s", hipGetErrorString(err));
+      return ok();
+    }
+  }
   GemmParams gl{};
   gl.A = lm_head;
   gl.lda = H;

@@ -495,6 +495,36 @@ __global__ __launch_bounds__(256) void argmax_partial_kernel(const float* logits
   }
 }
 
+// Pass 1 over row-major logits [R][ld]: workgroup c scans vocabulary chunk c
+// of every request; wave w takes requests w, w+4, ..., its lanes consecutive
+// entries (eight per lane in flight), and merges its lanes with shuffles.
+__global__ __launch_bounds__(256) void argmax_rows_partial_kernel(const float* logits, int64_t ld,
+                                                                  int vocab, int R, float2* partial) {
+  const int c = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int per = (vocab + ARGMAX_CHUNKS - 1) / ARGMAX_CHUNKS;
+  const int v0 = c * per, v1 = min(vocab, v0 + per);
+  for (int r = w; r < R; r += 4) {
+    const float* row = logits + (int64_t)r * ld;
+    float best = -INFINITY;
+    int bi = -1;
+    for (int vb = v0 + lane; vb < v1; vb += 8 * 64) {
+      float z[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) z[u] = vb + 64 * u < v1 ? row[vb + 64 * u] : 0.0f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (vb + 64 * u < v1) argmax_merge(best, bi, z[u], vb + 64 * u);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ob = __shfl_xor(best, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      argmax_merge(best, bi, ob, oi);
+    }
+    if (lane == 0) partial[(int64_t)c * R + r] = make_float2(best, __int_as_float(bi));
+  }
+}
+
 // Pass 2: one wave per request; lane l merges chunks l, l+64, ..., then the
 // wave merges its lanes.
 __global__ __launch_bounds__(64) void argmax_final_kernel(const float2* partial, int R,
@@ -569,6 +599,15 @@ void launch_argmax(const float* logits_t, int64_t ld, int vocab, int num_request
   if (num_requests <= 0) return;
   hipLaunchKernelGGL(argmax_partial_kernel, dim3(ARGMAX_CHUNKS), dim3(256), 0, s, logits_t, ld,
                      vocab, num_requests, partial, logits_out);
+  hipLaunchKernelGGL(argmax_final_kernel, dim3(num_requests), dim3(64), 0, s, partial,
+                     num_requests, next_tokens);
+}
+
+void launch_argmax_rows(const float* logits, int64_t ld, int vocab, int num_requests,
+                        float2* partial, int32_t* next_tokens, hipStream_t s) {
+  if (num_requests <= 0) return;
+  hipLaunchKernelGGL(argmax_rows_partial_kernel, dim3(ARGMAX_CHUNKS), dim3(256), 0, s, logits, ld,
+                     vocab, num_requests, partial);
   hipLaunchKernelGGL(argmax_final_kernel, dim3(num_requests), dim3(64), 0, s, partial,
                      num_requests, next_tokens);
 }

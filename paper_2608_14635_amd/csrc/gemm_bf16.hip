@@ -687,6 +687,27 @@ void launch_gemm_bf16_splitk(int epi, const GemmParams& p, float* part, int64_t 
     hipLaunchKernelGGL(splitk_epi_kernel<EPI_SWIGLU>, egrid, dim3(256), 0, s, q, tiles_n);
 }
 
+bool launch_gemm_bf16_rows(const GemmParams& p, float* out, int64_t ldo, hipStream_t s) {
+  const int N = p.n_end - p.n_begin;
+  if (!skinny_ok(p.M, p.K) || N <= 0) return false;
+  const int nbw = skinny_nbw(p.M);
+  if (N % (16 * nbw) != 0 || ldo < N) return false;
+  GemmParams q = p;
+  q.part = out;
+  q.part_ld = (int)ldo;
+  q.part_stride = 0;
+  q.ksplit = 1;
+  const int ngroups = N / 16 / nbw, kc_per = p.K / SK_CHUNK;
+  const dim3 grid((unsigned)((ngroups + 3) / 4)), block(256);
+  switch ((p.M + 15) / 16) {
+    case 1: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<1, 4>), grid, block, 0, s, q, ngroups, kc_per); break;
+    case 2: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<2, 2>), grid, block, 0, s, q, ngroups, kc_per); break;
+    case 3: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<3, 1>), grid, block, 0, s, q, ngroups, kc_per); break;
+    default: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<4, 1>), grid, block, 0, s, q, ngroups, kc_per); break;
+  }
+  return true;
+}
+
 void launch_gemm_bf16(int epi, const GemmParams& p_in, hipStream_t s) {
   const int tiles_m = (p_in.M + BM - 1) / BM;
   const int tiles_n = n_tiles_of(p_in);

@@ -88,6 +88,11 @@ void launch_gemm_f32(int epi, const GemmParams& p, hipStream_t s);
 void launch_gemm_bf16_splitk(int epi, const GemmParams& p, float* part, int64_t part_cap,
                              hipStream_t s);
 int64_t gemm_bf16_splitk_part_elems(int M, int N, int K);
+// Few-row product with K unsplit, fp32 C[M][N] = A . B^T written to out (row
+// stride ldo), no epilogue; B rows follow p.bmap as for the other products.
+// Returns false, launching nothing, unless M <= 64, K % 128 == 0 and N is a
+// multiple of the 16-row blocks a wave owns (64 for M <= 16).
+bool launch_gemm_bf16_rows(const GemmParams& p, float* out, int64_t ldo, hipStream_t s);
 
 // Attention.  qblk: per q-block int4 {q_start, q_len, req_start, 0} in
 // wave-local row indices, ordered longest-first.  Each request's rows start on
@@ -150,6 +155,9 @@ void launch_decode_attention(int dtype, const DecodeAttnParams& p, int num_reque
 constexpr int ARGMAX_CHUNKS = 256;  // vocab chunks of the first argmax pass
 void launch_argmax(const float* logits_t, int64_t ld, int vocab, int num_requests,
                    float2* partial, int32_t* next_tokens, float* logits_out, hipStream_t s);
+// The same greedy choice over row-major logits [num_requests][ld].
+void launch_argmax_rows(const float* logits, int64_t ld, int vocab, int num_requests,
+                        float2* partial, int32_t* next_tokens, hipStream_t s);
 
 // Block commit digests (flush-free recovery): one workgroup per entry reads
 // the entry's covered slots in every plane and reduces the keyed sum of squares.

@@ -36,12 +36,19 @@ SHAPES = {
     "qwen25_1_5b_2l": dataclasses.replace(W.QWEN25_1_5B.with_layers(2), vocab=2048),
     # 16 q heads per kv head
     "g16_bf16": dataclasses.replace(W.TINY_BF16, num_q_heads=32, num_kv_heads=2),
+    # a vocabulary of whole 64-row blocks: the LM head runs as a few-row
+    # product into row-major logits (the other bf16 vocabularies here take the
+    # transposed product)
+    "tiny_bf16_v1024": dataclasses.replace(W.TINY_BF16, vocab=1024),
 }
 # (shape, prefix lengths, block size): the default cases plus block size 32
 # and a batch of 40 requests (three 16-row tiles in the few-row products)
 CASES = {n: (n, None, 16) for n in SHAPES}
 CASES["tiny_bf16_b32"] = ("tiny_bf16", [1, 31, 32, 33, 97], 32)
 CASES["tiny_bf16_40req"] = ("tiny_bf16", [1 + (7 * i) % 90 for i in range(40)], 16)
+# the row-major LM head with two and three 16-row tiles of requests
+CASES["tiny_bf16_v1024_20req"] = ("tiny_bf16_v1024", [1 + (5 * i) % 60 for i in range(20)], 16)
+CASES["tiny_bf16_v1024_40req"] = ("tiny_bf16_v1024", [1 + (7 * i) % 90 for i in range(40)], 16)
 
 
 def say(msg):
@@ -75,13 +82,14 @@ class GpuDecoder:
         self.next = torch.zeros(R, dtype=torch.int32, device="cuda")
         self.logits = torch.zeros((R, wl.shape.vocab), dtype=torch.float32, device="cuda")
 
-    def step(self, arena, tokens, positions, rows=None):
+    def step(self, arena, tokens, positions, rows=None, want_logits=True):
         rows = np.arange(self.wl.num_requests) if rows is None else np.asarray(rows)
         n = len(rows)
         kvr.kv_decode_step(self.model.weights, self.head["final_norm"].data_ptr(),
                            self.head["lm_head"].data_ptr(), tokens, positions,
                            self.wl.block_tables[rows], arena.handle, self.ws.data_ptr(), self.nbytes,
-                           self.next.data_ptr(), self.logits.data_ptr(), Hn.stream_ptr())
+                           self.next.data_ptr(), self.logits.data_ptr() if want_logits else 0,
+                           Hn.stream_ptr())
         torch.cuda.synchronize()
         return self.next[:n].cpu().numpy().copy(), self.logits[:n].cpu().numpy().copy()
 
@@ -161,6 +169,11 @@ def test_decode_step_matches_oracle(oracle_lib, name):
     for r, p in enumerate(pos):
         m6[:, :, pre.block_tables[r, p // pre.block_size], p % pre.block_size] = False
     assert np.array_equal(after[mask], before[mask])
+    # the same step without a logits buffer: the same tokens, and it rewrites
+    # the same K/V rows
+    tok_n, _ = dec.step(arena, last, pos, want_logits=False)
+    assert np.array_equal(tok_n, tok_g)
+    assert np.array_equal(arena.to_host(), after)
 
 
 @pytest.mark.parametrize("name", ["tiny_f32", "tiny_bf16"])
