@@ -1172,13 +1172,20 @@ kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void
       launch_gemm_f32(epi, gp, st);
   };
   auto gemm_full = dt == KV_BF16 ? launch_gemm_bf16 : launch_gemm_f32;
+  // a residual product and the RMSNorm of the updated rows with `gain`: one
+  // kernel after the bf16 few-row product, else the product and the norm
+  auto resid_norm = [&](const GemmParams& gp, const void* gain) {
+    if (dt == KV_BF16 && launch_gemm_bf16_splitk_resid_norm(gp, gpart, L.gpart_elems, gain, A, eps, s))
+      return;
+    gemm(EPI_RESID, gp, s);
+    launch_rmsnorm(dt, X, gain, A, R, H, eps, s);
+  };
 
   // rope rows of the step's positions; the QKV epilogue indexes them by row
   launch_rope_rows(rope, d_pos, R, hd, d.rope_theta, s);
   launch_embed_norm(dt, w->embed, d_tok, w->layers[0].attn_norm, X, A, R, H, eps, s);
   for (int l = 0; l < d.num_layers; ++l) {
     const kv_layer_weights& lw = w->layers[l];
-    if (l > 0) launch_rmsnorm(dt, X, lw.attn_norm, A, R, H, eps, s);
     char* plane_k = abase + (int64_t)(2 * l) * plane * elem_bytes(dt);
     char* plane_v = abase + (int64_t)(2 * l + 1) * plane * elem_bytes(dt);
     GemmParams g{};
@@ -1241,8 +1248,7 @@ kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void
     go.n_end = H;
     go.epi.x = X;
     go.epi.ldx = H;
-    gemm(EPI_RESID, go, s);
-    launch_rmsnorm(dt, X, lw.ffn_norm, A, R, H, eps, s);
+    resid_norm(go, lw.ffn_norm);
     GemmParams gu{};
     gu.A = A;
     gu.lda = H;
@@ -1268,13 +1274,14 @@ kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void
     gd.n_end = H;
     gd.epi.x = X;
     gd.epi.ldx = H;
-    gemm(EPI_RESID, gd, s);
+    // the next layer's attention norm, or the final norm after the last layer
+    resid_norm(gd, l + 1 < d.num_layers ? w->layers[l + 1].attn_norm : final_norm);
   }
-  // final norm, LM head, argmax.  bf16: the few-row product writes row-major
-  // logits (into the caller's buffer when one is given); otherwise, and where
-  // the vocabulary is not a multiple of its blocks, the transposed product
-  // (vocab rows x padded request columns)
-  launch_rmsnorm(dt, X, final_norm, A, R, H, eps, s);
+  // LM head over the final-normed rows (the last layer's residual step wrote
+  // them), argmax.  bf16: the few-row product writes row-major logits (into
+  // the caller's buffer when one is given); otherwise, and where the
+  // vocabulary is not a multiple of its blocks, the transposed product (vocab
+  // rows x padded request columns)
   if (dt == KV_BF16) {
     GemmParams gr{};
     gr.A = A;

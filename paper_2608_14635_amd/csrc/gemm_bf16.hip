@@ -586,6 +586,65 @@ __global__ __launch_bounds__(256) void splitk_elem_kernel(GemmParams p) {
   }
 }
 
+// Residual sum and RMSNorm after a few-row product: workgroup m sums row m's
+// split-K partials in split order into the residual row X (the values
+// splitk_elem_kernel writes), then writes round(g * x / rms(x)) as the next
+// product's A row.  Every load (X, partials, gain) comes before any store.
+constexpr int RN_THREADS = 1024, RN_MAXI = 2;  // rows up to RN_THREADS * 4 * RN_MAXI wide
+__global__ __launch_bounds__(RN_THREADS) void splitk_resid_norm_kernel(GemmParams p, const bf16_t* gain,
+                                                                       bf16_t* a_out, float eps) {
+  __shared__ float red[RN_THREADS / 64];
+  const int m = blockIdx.x, tid = threadIdx.x;
+  const int N = p.n_end - p.n_begin;
+  float* xrow = p.epi.x + (int64_t)m * p.epi.ldx + p.n_begin;
+  const float* src[RN_MAXI];
+  bool valid[RN_MAXI];
+  float4 acc[RN_MAXI], xv[RN_MAXI];
+  uint2 gv[RN_MAXI];
+#pragma unroll
+  for (int i = 0; i < RN_MAXI; ++i) {
+    const int col = (tid + i * RN_THREADS) * 4;
+    valid[i] = col < N;
+    const int cc = valid[i] ? col : 0;
+    src[i] = p.part + (int64_t)m * p.part_ld + cc;
+    xv[i] = valid[i] ? *reinterpret_cast<const float4*>(xrow + cc) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    gv[i] = valid[i] ? *reinterpret_cast<const uint2*>(gain + cc) : make_uint2(0u, 0u);
+    acc[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  }
+  sum_splits<RN_MAXI, 8>(src, valid, p.ksplit, p.part_stride, acc);
+  float ss = 0.0f;
+#pragma unroll
+  for (int i = 0; i < RN_MAXI; ++i) {
+    if (!valid[i]) continue;
+    xv[i].x += acc[i].x;
+    xv[i].y += acc[i].y;
+    xv[i].z += acc[i].z;
+    xv[i].w += acc[i].w;
+    ss += xv[i].x * xv[i].x + xv[i].y * xv[i].y + xv[i].z * xv[i].z + xv[i].w * xv[i].w;
+  }
+#pragma unroll
+  for (int i = 0; i < RN_MAXI; ++i)
+    if (valid[i]) *reinterpret_cast<float4*>(xrow + (tid + i * RN_THREADS) * 4) = xv[i];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  float tot = 0.0f;
+#pragma unroll
+  for (int w = 0; w < RN_THREADS / 64; ++w) tot += red[w];
+  const float inv = 1.0f / sqrtf(tot / (float)N + eps);
+#pragma unroll
+  for (int i = 0; i < RN_MAXI; ++i) {
+    if (!valid[i]) continue;
+    const float g0 = __uint_as_float(gv[i].x << 16), g1 = __uint_as_float(gv[i].x & 0xffff0000u);
+    const float g2 = __uint_as_float(gv[i].y << 16), g3 = __uint_as_float(gv[i].y & 0xffff0000u);
+    uint2 o;
+    o.x = (uint32_t)f2bf(g0 * xv[i].x * inv) | ((uint32_t)f2bf(g1 * xv[i].y * inv) << 16);
+    o.y = (uint32_t)f2bf(g2 * xv[i].z * inv) | ((uint32_t)f2bf(g3 * xv[i].w * inv) << 16);
+    *reinterpret_cast<uint2*>(a_out + (int64_t)m * N + (tid + i * RN_THREADS) * 4) = o;
+  }
+}
+
 struct SkinnyPlan {
   int nbw, ngroups, ksplit, kc_per;
 };
@@ -608,6 +667,17 @@ SkinnyPlan skinny_plan(int M, int tiles_n, int K, int max_split) {
   sp.kc_per = (KC + want - 1) / want;
   sp.ksplit = (KC + sp.kc_per - 1) / sp.kc_per;
   return sp;
+}
+
+// q.ksplit K ranges of kc_per chunks over ngroups groups of 16-row blocks
+void launch_skinny(const GemmParams& q, int ngroups, int kc_per, hipStream_t s) {
+  const dim3 grid((unsigned)((ngroups * q.ksplit + 3) / 4)), block(256);
+  switch ((q.M + 15) / 16) {
+    case 1: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<1, 4>), grid, block, 0, s, q, ngroups, kc_per); break;
+    case 2: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<2, 2>), grid, block, 0, s, q, ngroups, kc_per); break;
+    case 3: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<3, 1>), grid, block, 0, s, q, ngroups, kc_per); break;
+    default: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<4, 1>), grid, block, 0, s, q, ngroups, kc_per); break;
+  }
 }
 
 struct SplitPlan {
@@ -656,13 +726,7 @@ void launch_gemm_bf16_splitk(int epi, const GemmParams& p, float* part, int64_t 
   if (skinny_ok(p.M, p.K) && (int64_t)skinny_plan(p.M, tiles_n, p.K, max_split).ksplit * p.M * ld <= part_cap) {
     const SkinnyPlan kp = skinny_plan(p.M, tiles_n, p.K, max_split);
     q.ksplit = kp.ksplit;
-    const dim3 grid((unsigned)((kp.ngroups * kp.ksplit + 3) / 4)), block(256);
-    switch ((p.M + 15) / 16) {
-      case 1: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<1, 4>), grid, block, 0, s, q, kp.ngroups, kp.kc_per); break;
-      case 2: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<2, 2>), grid, block, 0, s, q, kp.ngroups, kp.kc_per); break;
-      case 3: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<3, 1>), grid, block, 0, s, q, kp.ngroups, kp.kc_per); break;
-      default: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<4, 1>), grid, block, 0, s, q, kp.ngroups, kp.kc_per); break;
-    }
+    launch_skinny(q, kp.ngroups, kp.kc_per, s);
   } else {
     const SplitPlan sp = split_plan(p.M, tiles_n, p.K);
     if (sp.ksplit <= 1 || (int64_t)sp.ksplit * p.M * ld > part_cap) {
@@ -687,6 +751,27 @@ void launch_gemm_bf16_splitk(int epi, const GemmParams& p, float* part, int64_t 
     hipLaunchKernelGGL(splitk_epi_kernel<EPI_SWIGLU>, egrid, dim3(256), 0, s, q, tiles_n);
 }
 
+bool launch_gemm_bf16_splitk_resid_norm(const GemmParams& p, float* part, int64_t part_cap,
+                                        const void* gain, void* a_out, float eps, hipStream_t s) {
+  const int N = p.n_end - p.n_begin;
+  if (p.bmap != BMAP_PLAIN || !skinny_ok(p.M, p.K) || N <= 0 || N % BN != 0 ||
+      N > RN_THREADS * 4 * RN_MAXI)
+    return false;
+  const int tiles_n = N / BN;
+  const int64_t ld = (int64_t)tiles_n * BN;
+  const SkinnyPlan kp = skinny_plan(p.M, tiles_n, p.K, SK_MAX_SPLIT_ELEM);
+  if ((int64_t)kp.ksplit * p.M * ld > part_cap) return false;
+  GemmParams q = p;
+  q.part = part;
+  q.part_ld = (int)ld;
+  q.part_stride = (int64_t)p.M * ld;
+  q.ksplit = kp.ksplit;
+  launch_skinny(q, kp.ngroups, kp.kc_per, s);
+  hipLaunchKernelGGL(splitk_resid_norm_kernel, dim3((unsigned)p.M), dim3(RN_THREADS), 0, s, q,
+                     (const bf16_t*)gain, (bf16_t*)a_out, eps);
+  return true;
+}
+
 bool launch_gemm_bf16_rows(const GemmParams& p, float* out, int64_t ldo, hipStream_t s) {
   const int N = p.n_end - p.n_begin;
   if (!skinny_ok(p.M, p.K) || N <= 0) return false;
@@ -698,13 +783,7 @@ bool launch_gemm_bf16_rows(const GemmParams& p, float* out, int64_t ldo, hipStre
   q.part_stride = 0;
   q.ksplit = 1;
   const int ngroups = N / 16 / nbw, kc_per = p.K / SK_CHUNK;
-  const dim3 grid((unsigned)((ngroups + 3) / 4)), block(256);
-  switch ((p.M + 15) / 16) {
-    case 1: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<1, 4>), grid, block, 0, s, q, ngroups, kc_per); break;
-    case 2: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<2, 2>), grid, block, 0, s, q, ngroups, kc_per); break;
-    case 3: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<3, 1>), grid, block, 0, s, q, ngroups, kc_per); break;
-    default: hipLaunchKernelGGL((gemm_bf16_skinny_kernel<4, 1>), grid, block, 0, s, q, ngroups, kc_per); break;
-  }
+  launch_skinny(q, ngroups, kc_per, s);
   return true;
 }
 

@@ -88,6 +88,13 @@ void launch_gemm_f32(int epi, const GemmParams& p, hipStream_t s);
 void launch_gemm_bf16_splitk(int epi, const GemmParams& p, float* part, int64_t part_cap,
                              hipStream_t s);
 int64_t gemm_bf16_splitk_part_elems(int M, int N, int K);
+// Few-row product into the residual stream followed by the RMSNorm of the
+// updated rows: X[m] += A[m] . B^T (split-K sums in split order, as
+// launch_gemm_bf16_splitk with EPI_RESID), then a_out[m] = round(gain * X[m] /
+// rms(X[m])) (bf16, row stride N).  Returns false, launching nothing, where
+// the few-row kernel or the row width does not apply.
+bool launch_gemm_bf16_splitk_resid_norm(const GemmParams& p, float* part, int64_t part_cap,
+                                        const void* gain, void* a_out, float eps, hipStream_t s);
 // Few-row product with K unsplit, fp32 C[M][N] = A . B^T written to out (row
 // stride ldo), no epilogue; B rows follow p.bmap as for the other products.
 // Returns false, launching nothing, unless M <= 64, K % 128 == 0 and N is a
