@@ -430,31 +430,33 @@ __device__ __forceinline__ void sum_splits(const float* const (&src)[IPT], const
   }
 }
 
-template <int EPI>
+// TW: the epilogue's tile width, BN or (QKV, head dim dividing 128) 128 for
+// twice the workgroups
+template <int EPI, int TW>
 __global__ __launch_bounds__(256) void splitk_epi_kernel(GemmParams p, int tiles_n) {
   __shared__ __attribute__((aligned(16))) float sC[SK_ROWS * LDC];
   const int tile_n = blockIdx.x % tiles_n, m0 = (blockIdx.x / tiles_n) * SK_ROWS;
   const int tid = threadIdx.x;
-  constexpr int IPT = SK_ROWS * (BN / 4) / 256;
+  constexpr int IPT = SK_ROWS * (TW / 4) / 256;
   const float* src[IPT];
   bool valid[IPT];
   float4 a[IPT];
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    const int it = tid + i * 256, r = it / (BN / 4), c = (it % (BN / 4)) * 4;
+    const int it = tid + i * 256, r = it / (TW / 4), c = (it % (TW / 4)) * 4;
     valid[i] = m0 + r < p.M;
-    src[i] = p.part + (int64_t)min(m0 + r, p.M - 1) * p.part_ld + tile_n * BN + c;
+    src[i] = p.part + (int64_t)min(m0 + r, p.M - 1) * p.part_ld + tile_n * TW + c;
     a[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
   }
   sum_splits<IPT, 4>(src, valid, p.ksplit, p.part_stride, a);
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    const int it = tid + i * 256, r = it / (BN / 4), c = (it % (BN / 4)) * 4;
+    const int it = tid + i * 256, r = it / (TW / 4), c = (it % (TW / 4)) * 4;
     *reinterpret_cast<float4*>(sC + r * LDC + c) = a[i];
   }
   __syncthreads();
   if (EPI == EPI_QKV) {
-    epi_qkv<bf16_t, BN, 256>(sC, LDC, SK_ROWS, m0, p.M, p.n_begin + tile_n * BN, p.epi);
+    epi_qkv<bf16_t, TW, 256>(sC, LDC, SK_ROWS, m0, p.M, p.n_begin + tile_n * TW, p.epi);
   } else if (EPI == EPI_RESID) {
     epi_resid<BN, 256>(sC, LDC, SK_ROWS, m0, p.M, p.n_begin + tile_n * BN, p.epi);
   } else if (EPI == EPI_STORE) {
@@ -741,14 +743,18 @@ void launch_gemm_bf16_splitk(int epi, const GemmParams& p, float* part, int64_t 
   }
   const dim3 egrid((unsigned)(((p.M + SK_ROWS - 1) / SK_ROWS) * tiles_n));
   const dim3 lgrid((unsigned)(((int64_t)p.M * (ld / 4) + 255) / 256));
-  if (epi == EPI_QKV)
-    hipLaunchKernelGGL(splitk_epi_kernel<EPI_QKV>, egrid, dim3(256), 0, s, q, tiles_n);
+  if (epi == EPI_QKV && p.epi.d > 0 && 128 % p.epi.d == 0) {
+    const int tiles_h = tiles_n * (BN / 128);
+    const dim3 hgrid((unsigned)(((p.M + SK_ROWS - 1) / SK_ROWS) * tiles_h));
+    hipLaunchKernelGGL((splitk_epi_kernel<EPI_QKV, 128>), hgrid, dim3(256), 0, s, q, tiles_h);
+  } else if (epi == EPI_QKV)
+    hipLaunchKernelGGL((splitk_epi_kernel<EPI_QKV, BN>), egrid, dim3(256), 0, s, q, tiles_n);
   else if (epi == EPI_RESID)
     hipLaunchKernelGGL(splitk_elem_kernel<EPI_RESID>, lgrid, dim3(256), 0, s, q);
   else if (epi == EPI_STORE)
     hipLaunchKernelGGL(splitk_elem_kernel<EPI_STORE>, lgrid, dim3(256), 0, s, q);
   else
-    hipLaunchKernelGGL(splitk_epi_kernel<EPI_SWIGLU>, egrid, dim3(256), 0, s, q, tiles_n);
+    hipLaunchKernelGGL((splitk_epi_kernel<EPI_SWIGLU, BN>), egrid, dim3(256), 0, s, q, tiles_n);
 }
 
 bool launch_gemm_bf16_splitk_resid_norm(const GemmParams& p, float* part, int64_t part_cap,
