@@ -217,7 +217,8 @@ __global__ __launch_bounds__(DNT) void decode_attn_kernel(DecodeAttnParams p) {
 // of 16 keys (a tile never crosses an arena block when the block size is a
 // multiple of 16).  Each lane loads 16-byte pieces of the keys' K and V rows
 // straight into registers (a key's 256-byte head slice is four lanes' worth
-// per instruction), and the next tile is in flight while this one is used.
+// per instruction); the next tile's loads are issued before this tile's
+// products (the copy into place at the end of the tile waits for them).
 // Scores: S^T = K Q^T on v_mfma_f32_16x16x32_bf16 with the g q heads as the
 // 16 columns (unused columns hold zero queries): lane (q, c) = (lane/16,
 // lane%16) gets keys 4q..4q+3 of head c.  Online softmax per head in the exp2
