@@ -49,6 +49,12 @@ CASES["tiny_bf16_40req"] = ("tiny_bf16", [1 + (7 * i) % 90 for i in range(40)], 
 # the row-major LM head with two and three 16-row tiles of requests
 CASES["tiny_bf16_v1024_20req"] = ("tiny_bf16_v1024", [1 + (5 * i) % 60 for i in range(20)], 16)
 CASES["tiny_bf16_v1024_40req"] = ("tiny_bf16_v1024", [1 + (7 * i) % 90 for i in range(40)], 16)
+# the edges of the few-row products: one full 16-row tile, their largest batch
+# (64 rows), and one request more (the general split-K path, with the residual
+# sum and the norm as separate kernels)
+CASES["tiny_bf16_v1024_16req"] = ("tiny_bf16_v1024", [1 + (11 * i) % 70 for i in range(16)], 16)
+CASES["tiny_bf16_v1024_64req"] = ("tiny_bf16_v1024", [1 + (13 * i) % 50 for i in range(64)], 16)
+CASES["tiny_bf16_v1024_65req"] = ("tiny_bf16_v1024", [1 + (13 * i) % 50 for i in range(65)], 16)
 
 
 def say(msg):
