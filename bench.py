@@ -62,6 +62,22 @@ def measured_traffic(kernel: str, workload: str):
     return rec.get("bytes_per_launch")
 
 
+def decode_step_bytes(s, ctx_lens) -> int:
+    """Algorithmic HBM bytes of one decode step over requests whose contexts
+    (the step's own position included) have the lengths ctx_lens: every layer's
+    weights (Q/K/V/O and gate/up/down projections, both norm gains), the final
+    norm gain and the LM head once; each request's embedding row; every
+    context key's K and V row once per layer; the step's new K and V rows."""
+    e = s.elem_bytes
+    H, F, d, nq, nkv, L = s.hidden, s.ffn_dim, s.head_dim, s.num_q_heads, s.num_kv_heads, s.num_layers
+    R = len(ctx_lens)
+    w_layer = (H * (nq + 2 * nkv) * d + nq * d * H + 3 * H * F + 2 * H) * e
+    weights = L * w_layer + (s.vocab * H + H) * e + R * H * e
+    kv_read = int(sum(int(n) for n in ctx_lens)) * L * 2 * nkv * d * e
+    kv_write = R * L * 2 * nkv * d * e
+    return weights + kv_read + kv_write
+
+
 def resume_decode(wl, model, arena, Hn, kvr, W, steps, stream, log):
     """Resumed generation over the rebuilt arena: one greedy decode step per
     request, timed with HIP events.  Each step decodes every request's last
@@ -96,13 +112,7 @@ def resume_decode(wl, model, arena, Hn, kvr, W, steps, stream, log):
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
-    e = s.elem_bytes
-    H, F, d, nq, nkv, L = s.hidden, s.ffn_dim, s.head_dim, s.num_q_heads, s.num_kv_heads, s.num_layers
-    w_layer = (H * (nq + 2 * nkv) * d + nq * d * H + 3 * H * F + 2 * H) * e
-    weights = L * w_layer + (s.vocab * H + H) * e + len(rows) * H * e
-    kv_read = int(lens[rows].sum()) * L * 2 * nkv * d * e
-    kv_write = len(rows) * L * 2 * nkv * d * e
-    total = weights + kv_read + kv_write
+    total = decode_step_bytes(s, lens[rows])
     out = {"steps": steps, "requests": int(len(rows)), "ms_per_step": ms,
            "tokens_per_s": len(rows) / (ms / 1e3), "context_tokens": int(lens[rows].sum()),
            "hbm_bytes_per_step": total, "achieved_GBps": total / (ms / 1e3) / 1e9,

@@ -66,3 +66,27 @@ def test_linear_flops_per_token_of_the_8b_shape():
     # measurement plan states for the benchmark configuration)
     wl = types.SimpleNamespace(shape=W.LLAMA8B, lens=np.array([1]), total_tokens=1)
     assert abs(bench.algorithmic_work(wl)["linear_flops"] / 1e9 - 13.54) < 0.005
+
+
+def test_decode_step_bytes_recounted():
+    # one decode step: each weight matrix element and gain once, the LM head
+    # and final gain once, one embedding row per request, and per layer the K
+    # and V rows of every context key (brute-force over keys) plus the new rows
+    for s in (W.LLAMA8B, W.QWEN3_8B, W.TINY_BF16):
+        ctx = [1, 7, 300]
+        e, L = s.elem_bytes, s.num_layers
+        mats = sum(o * i for o, i in _matrices(s, False)) * L
+        gains = 2 * s.hidden * L + s.hidden
+        head = s.vocab * s.hidden
+        emb = len(ctx) * s.hidden
+        row = s.num_kv_heads * s.head_dim
+        kv = sum(1 for n in ctx for _ in range(n)) * L * 2 * row
+        new = len(ctx) * L * 2 * row
+        assert bench.decode_step_bytes(s, ctx) == (mats + gains + head + emb + kv + new) * e
+
+
+def test_decode_step_bytes_of_the_8b_benchmark():
+    # the figure the benchmark prices the decode step with: 16 requests over
+    # the 8B workload's 128,325 context tokens
+    wl = W.config2()
+    assert bench.decode_step_bytes(W.LLAMA8B, wl.lens) == 31831891968
