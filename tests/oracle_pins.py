@@ -442,12 +442,17 @@ def pin_torch_variants_f64(o):
 
 
 def pin_torch_variants_rounding(o):
+    """The variants' rounding sites (bias joined to the fp64 sum before its one
+    rounding to fp32; the head norm's output kept in working precision until q
+    and k are rounded after RoPE) against the torch forward with the same
+    sites emulated, held to the base model's bar: the bound and the share of
+    bit-identical values of pin_torch_f32_rounding / pin_torch_bf16_rounding."""
     for name, kw in VARIANTS.items():
-        for base, rounding, tol in ((dataclasses.replace(TINY_GQA, **kw), "f32", 1e-5),
-                                    (dataclasses.replace(TINY_BF16_2L, **kw), "bf16", 2e-2)):
+        for base, rounding, tol in ((dataclasses.replace(TINY_GQA, **kw), "f32", 1e-6),
+                                    (dataclasses.replace(TINY_BF16_2L, **kw), "bf16", 1e-3)):
             wl = W.small_workload(base, [5, 19], seed=151, other_live_frac=0.0)
             w = W.host_weights(base, seed=52)
-            _torch_compare(o, base, wl, w, base.dtype, rounding, tol)
+            _torch_compare(o, base, wl, w, base.dtype, rounding, tol, min_exact=0.999)
 
 
 def pin_qk_norm_scale_invariance(o):

@@ -69,6 +69,20 @@ MUTANTS = [
      "if (dg == committed[e]) intact[r] += 1;", 0),
     ("verify_tail_block_full", "const int32_t n = lens[r] - j * B < B ? lens[r] - j * B : B;",
      "const int32_t n = B;", 0),
+    # rounding sites of the Qwen variants
+    ("qk_norm_output_rounded_before_rope", "for (e = 0; e < d; ++e) hu[e] = to_work(load(g, dt, e) * hu[e] * inv, dt);",
+     "for (e = 0; e < d; ++e) hu[e] = rnd(load(g, dt, e) * hu[e] * inv, dt);", 0),
+    ("bias_added_after_rounding", "to_work(dot_row(W, dt, i, K, A + r * K) + load(b, dt, i), dt)",
+     "to_work(to_work(dot_row(W, dt, i, K, A + r * K), dt) + load(b, dt, i), dt)", 0),
+    ("qk_norm_gain_after_rope", [
+        ("for (e = 0; e < d; ++e) hu[e] = to_work(load(g, dt, e) * hu[e] * inv, dt);",
+         "for (e = 0; e < d; ++e) hu[e] = to_work(hu[e] * inv, dt);", 0),
+        ("rope_row(k + r * nkv * d, (int)nkv, (int)d, p, m->rope_theta, dt);",
+         "rope_row(k + r * nkv * d, (int)nkv, (int)d, p, m->rope_theta, dt);\n"
+         "    if (m->qk_norm) {\n"
+         "      for (e = 0; e < nq * d; ++e) q[r * nq * d + e] = to_work(load(lw->q_norm, dt, e % d) * q[r * nq * d + e], dt);\n"
+         "      for (e = 0; e < nkv * d; ++e) k[r * nkv * d + e] = to_work(load(lw->k_norm, dt, e % d) * k[r * nkv * d + e], dt);\n"
+         "    }", 0)], None, None),
     ("round_p_ignored", "if (m->round_p) z[j] = rnd(to_work(z[j], dt), dt);", "", 0),
     ("round_p_denominator_unrounded",
      "      if (m->round_p) z[j] = rnd(to_work(z[j], dt), dt);\n      den += z[j];",
@@ -77,6 +91,10 @@ MUTANTS = [
 
 
 def _patch(text, old, new, occ):
+    if isinstance(old, list):  # several sites: a list of (old, new, occurrence)
+        for o, n, k in old:
+            text = _patch(text, o, n, k)
+        return text
     idx = -1
     for _ in range(occ + 1):
         idx = text.find(old, idx + 1)
