@@ -27,11 +27,17 @@
  * to fp32 before the next op; rnd() is the identity for fp32 models and
  * fp32 -> bf16 round-to-nearest-even for bf16 models.  KVO_F64 rounds nothing.
  *
- * Optional mode round_p: the attention weights w_j = exp(z_j - max z) are
- * rounded like an op output (rnd(fp32(w_j))) before both the weighted sum of
- * V^ and the denominator.  It models a freedom the GPU path declares (its
- * P.V product takes P in the model dtype); the definition above is the mode
- * off.
+ * Optional mode round_p: the attention weights are rounded like an op output
+ * before both the weighted sum of V^ and the denominator.  Softmax is
+ * unchanged by scaling every weight of a row by one factor, and rounding to
+ * fp32 or bf16 commutes with scaling by a power of two, so the weights are
+ * taken relative to a power of two of the row maximum: with c = ceil(max_j
+ * z_j log2 e), w_j = rnd(fp32(2^(z_j log2 e - c))).  The result then does not
+ * depend on which power of two anchors the row (any integer c gives the same
+ * rounded weights up to that factor), which is what lets an online softmax
+ * that raises its anchor tile by tile round exactly these weights.  It models
+ * a freedom the GPU path declares (its P.V product takes P in the model
+ * dtype); the definition above is the mode off.
  */
 #include "kvo.h"
 
@@ -257,10 +263,17 @@ static void layer_step(const kvo_model* m, const kvo_layer* lw, int l, double* x
       z[j] = s * scale;
       if (z[j] > zmax) zmax = z[j];
     }
-    for (j = 0; j <= p; ++j) {
-      z[j] = exp(z[j] - zmax);
-      if (m->round_p) z[j] = rnd(to_work(z[j], dt), dt);
-      den += z[j];
+    if (m->round_p) {
+      const double c = ceil(zmax * M_LOG2E);
+      for (j = 0; j <= p; ++j) {
+        z[j] = rnd(to_work(exp2(z[j] * M_LOG2E - c), dt), dt);
+        den += z[j];
+      }
+    } else {
+      for (j = 0; j <= p; ++j) {
+        z[j] = exp(z[j] - zmax);
+        den += z[j];
+      }
     }
     for (e = 0; e < d; ++e) {
       double o = 0.0;

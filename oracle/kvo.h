@@ -41,8 +41,10 @@ typedef struct {
   int32_t dtype;         /* element type of weights and arena: KVO_F32/BF16/F64 */
   int32_t qk_norm;       /* 1: per-head RMSNorm of q and k before RoPE (Qwen3)   */
   int32_t qkv_bias;      /* 1: q, k, v projections carry a bias (Qwen2.5)        */
-  int32_t round_p;       /* 1: attention weights P = exp(z - max z) rounded to the
-                            model dtype before the P.V sum and the denominator
+  int32_t round_p;       /* 1: attention weights rounded to the model dtype
+                            before the P.V sum and the denominator, each weight
+                            exp(z - max z) scaled by a power of two first:
+                            P_j = rnd(2^(z_j log2 e - c)), c = ceil(max z log2 e)
                             (the GPU's declared freedom; 0 = the definition)   */
 } kvo_model;
 

@@ -15,8 +15,9 @@
 // every V^T operand is one 16-byte LDS read.  exp2 with the scale folded in;
 // P rounded to bf16 for the MFMA, and the softmax denominator summed from
 // the same rounded values (bf16 dot2 with fp32 accumulation); fp32 accumulation; masking only on tiles
-// that cross a wave's diagonal; the O rescale runs only when some lane's
-// max rose by a factor above 2^8 since the last one.  q-blocks are
+// that cross a wave's diagonal; the exponents are taken against an integer
+// anchor (log2 units), raised and O rescaled by a power of two only when
+// some lane's max rose by a factor above 2^8 since the last rescale.  q-blocks are
 // scheduled longest-first.  Deterministic: fixed key order, no atomics.
 //
 // fp32 path: a plain online-softmax kernel (one wave per query, lanes across
@@ -207,11 +208,14 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       // The reference max used for the exponents may lag the true running
       // max by up to RESCALE_SLACK (log2 units): P then reaches at most
       // 2^RESCALE_SLACK, which the fp32 sums and the final division by l
-      // absorb exactly, and P's bf16 rounding is relative, so nothing changes
-      // in accuracy while the 64-register rescale of O runs on few tiles.
+      // absorb exactly, while the 64-register rescale of O runs on few tiles.
+      // The reference is an integer (the max rounded up), so every rescale
+      // factor is an exact power of two and each key's rounded weight equals
+      // bf16(2^(s - c)) for the row's final anchor c, whichever tile raised
+      // it: rounding to bf16 commutes with scaling by a power of two.
       if (__any(mx > m_run + RESCALE_SLACK)) {
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        const float m_new = ceilf(fmaxf(m_run, mx));
+        const float alpha = m_run == -INFINITY ? 0.0f : ldexpf(1.0f, (int)(m_run - m_new));
         l_run *= alpha;
 #pragma unroll
         for (int t = 0; t < D / 32; ++t)

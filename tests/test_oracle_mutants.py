@@ -83,10 +83,12 @@ MUTANTS = [
          "      for (e = 0; e < nq * d; ++e) q[r * nq * d + e] = to_work(load(lw->q_norm, dt, e % d) * q[r * nq * d + e], dt);\n"
          "      for (e = 0; e < nkv * d; ++e) k[r * nkv * d + e] = to_work(load(lw->k_norm, dt, e % d) * k[r * nkv * d + e], dt);\n"
          "    }", 0)], None, None),
-    ("round_p_ignored", "if (m->round_p) z[j] = rnd(to_work(z[j], dt), dt);", "", 0),
+    ("round_p_ignored", "z[j] = rnd(to_work(exp2(z[j] * M_LOG2E - c), dt), dt);", "z[j] = exp2(z[j] * M_LOG2E - c);", 0),
     ("round_p_denominator_unrounded",
-     "      if (m->round_p) z[j] = rnd(to_work(z[j], dt), dt);\n      den += z[j];",
-     "      den += z[j];\n      if (m->round_p) z[j] = rnd(to_work(z[j], dt), dt);", 0),
+     "        z[j] = rnd(to_work(exp2(z[j] * M_LOG2E - c), dt), dt);\n        den += z[j];",
+     "        den += exp2(z[j] * M_LOG2E - c);\n        z[j] = rnd(to_work(exp2(z[j] * M_LOG2E - c), dt), dt);", 0),
+    ("round_p_anchored_at_the_exact_max", "const double c = ceil(zmax * M_LOG2E);",
+     "const double c = zmax * M_LOG2E;", 0),
 ]
 
 

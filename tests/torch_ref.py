@@ -38,8 +38,9 @@ def forward(shape: W.ModelShape, w64: Dict, tokens: np.ndarray,
             ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
     """One request.  Returns K [L, n, nkv, d], V [L, n, nkv, d] (rounded as
     stored) and the final residual [n, H].  round_p: attention written out
-    as softmax weights exp(z - max z), rounded like an op output, then
-    (P V) / sum(P), instead of scaled_dot_product_attention."""
+    as softmax weights 2^(z log2 e - c) with c the row max in log2 units
+    rounded up, rounded like an op output, then (P V) / sum(P), instead of
+    scaled_dot_product_attention."""
     n = len(tokens)
     H, d, nq, nkv = shape.hidden, shape.head_dim, shape.num_q_heads, shape.num_kv_heads
 
@@ -85,7 +86,9 @@ def forward(shape: W.ModelShape, w64: Dict, tokens: np.ndarray,
             vh = v.transpose(0, 1).repeat_interleave(g, dim=0)
             z = torch.matmul(qh, kh.transpose(1, 2).contiguous()) / math.sqrt(d)
             z = z.masked_fill(torch.triu(torch.ones(n, n, dtype=torch.bool), 1), float("-inf"))
-            pw = rnd(work(torch.exp(z - z.amax(dim=-1, keepdim=True))))
+            # weights relative to a power of two of the row max (log2 units)
+            c = torch.ceil(z.amax(dim=-1, keepdim=True) * (1.0 / math.log(2.0)))
+            pw = rnd(work(torch.exp2(z * (1.0 / math.log(2.0)) - c)))
             o = (torch.matmul(pw, vh) / pw.sum(dim=-1, keepdim=True))[None]
         else:
             o = F.scaled_dot_product_attention(q.transpose(0, 1)[None], k.transpose(0, 1)[None],
