@@ -82,6 +82,26 @@ def device_model_random(shape: W.ModelShape, seed: int = 1234, device="cuda",
     return DeviceModel(shape, embed, layers, _bind_weights(shape, embed, layers))
 
 
+def model_view(shape: W.ModelShape, embed: torch.Tensor, layers: List[Dict[str, torch.Tensor]]) -> DeviceModel:
+    """A model over existing device tensors (an embedding table and layer weights)."""
+    return DeviceModel(shape, embed, layers, _bind_weights(shape, embed, layers))
+
+
+def upload(shape: W.ModelShape, a: np.ndarray, device="cuda") -> torch.Tensor:
+    """A host array in oracle format (bf16 bits or fp32) as a device tensor of the model dtype."""
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if shape.dtype == W.BF16:
+        t = t.view(torch.int16).view(torch.bfloat16)
+    return t.to(device)
+
+
+def first_layers(model: DeviceModel, n: int) -> DeviceModel:
+    """The same device weights seen as an n-layer model (its first n layers)."""
+    shape = model.shape.with_layers(n)
+    layers = model.layers[:n]
+    return DeviceModel(shape, model.embed, layers, _bind_weights(shape, model.embed, layers))
+
+
 def device_head_from_host(shape: W.ModelShape, head: Dict, device="cuda") -> Dict[str, torch.Tensor]:
     """Final-norm gain and LM head of the resumed decode (workloads.host_head_weights) on the device."""
     out = {}
@@ -118,6 +138,16 @@ def host_copy_all(model: DeviceModel) -> Dict:
     """All weights back on the host in oracle format (small models only)."""
     return {"embed": _down(model, model.embed),
             "layers": [{k: _down(model, v) for k, v in lw.items()} for lw in model.layers]}
+
+
+def host_copy_head(model: DeviceModel, head: Dict[str, torch.Tensor]) -> Dict:
+    """Final-norm gain and LM head back on the host in oracle format."""
+    return {k: _down(model, v) for k, v in head.items()}
+
+
+def host_copy_layer(model: DeviceModel, l: int) -> Dict:
+    """Layer l's weights back on the host in oracle format."""
+    return {k: _down(model, v) for k, v in model.layers[l].items()}
 
 
 def host_copy_layer0(model: DeviceModel) -> Dict:

@@ -40,6 +40,9 @@ SHAPES = {
     # product into row-major logits (the other bf16 vocabularies here take the
     # transposed product)
     "tiny_bf16_v1024": dataclasses.replace(W.TINY_BF16, vocab=1024),
+    # two layers of the small decoder, for long contexts the oracle still
+    # rebuilds in seconds
+    "tiny_bf16_2l": W.TINY_BF16.with_layers(2),
 }
 # (shape, prefix lengths, block size): the default cases plus block size 32
 # and a batch of 40 requests (three 16-row tiles in the few-row products)
@@ -55,6 +58,10 @@ CASES["tiny_bf16_v1024_40req"] = ("tiny_bf16_v1024", [1 + (7 * i) % 90 for i in 
 CASES["tiny_bf16_v1024_16req"] = ("tiny_bf16_v1024", [1 + (11 * i) % 70 for i in range(16)], 16)
 CASES["tiny_bf16_v1024_64req"] = ("tiny_bf16_v1024", [1 + (13 * i) % 50 for i in range(64)], 16)
 CASES["tiny_bf16_v1024_65req"] = ("tiny_bf16_v1024", [1 + (13 * i) % 50 for i in range(65)], 16)
+# long contexts: 8192 keys split into 128 ranges of 64 keys (the split's cap),
+# a ragged 5000-key context, and 16 requests of 1-2K keys (31 ranges each)
+CASES["tiny_bf16_2l_long"] = ("tiny_bf16_2l", [8192, 5000, 1], 16)
+CASES["tiny_bf16_2l_16req_1k_2k"] = ("tiny_bf16_2l", [1024 + 61 * i for i in range(16)], 16)
 
 
 def say(msg):

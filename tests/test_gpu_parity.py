@@ -244,46 +244,6 @@ def test_real_width_two_layers(oracle_lib, name, B):
 
 
 # --------------------------------------------------------------------------
-# the 8B shape through all 32 layers (short requests: the oracle's full-depth
-# cost is about 0.44 GFLOP per token per layer)
-# --------------------------------------------------------------------------
-def test_8b_all_layers(oracle_lib):
-    """Random-weight layers amplify rounding differences with depth, so at
-    full depth the bar is set by the oracle itself: the same oracle with P
-    rounded to bf16 before P.V (the GPU's declared freedom) drifts from the
-    plain one by a measured amount per layer; the GPU must stay within the
-    stated tolerance over the first 8 layers and within 1.5x that drift
-    (plus 5e-3) everywhere.  A kernel mistake (index, sign, position) shows
-    up as errors of order 1, far above either bar."""
-    shape = W.LLAMA8B
-    wl = W.small_workload(shape, [1, 17, 40], block_size=16, seed=411, other_live_frac=0.3)
-    say(f"llama8b all {shape.num_layers} layers lens={wl.lens.tolist()}")
-    model = Hn.device_model_random(shape, seed=412, gain_std=0.1)
-    host_w = Hn.host_copy_all(model)
-    image = W.host_arena(wl)
-    g, arena = gpu_rebuild(wl, model, host_image=image)
-    arena.release()
-    del model
-    torch.cuda.empty_cache()
-    say("  oracle, all layers")
-    o = oracle_rebuild(oracle_lib, wl, host_w, image)
-    say("  oracle with P rounded to bf16, all layers")
-    o_p = image.copy()
-    oracle_lib.rebuild(shape, host_w, wl.tokens, wl.lens, wl.block_tables, o_p, wl.block_size,
-                       wl.num_blocks, round_p=True)
-    gpu_err, rep = PU.compare(wl, g, o, image)
-    drift, _ = PU.compare(wl, o_p, o, image)
-    np.set_printoptions(precision=3, linewidth=220)
-    say(f"  GPU vs oracle per layer (K, V max): {gpu_err.max(axis=1)}")
-    say(f"  oracle(P in bf16) vs oracle:        {drift.max(axis=1)}")
-    assert rep["unwritten_changed"] == 0 and rep["written_nonfinite"] == 0
-    tol = PU.TOL[W.BF16]
-    assert gpu_err[:8].max() <= tol, gpu_err[:8]
-    bound = np.maximum(tol, 1.5 * drift + 5e-3)
-    assert np.all(gpu_err <= bound), (gpu_err, bound)
-
-
-# --------------------------------------------------------------------------
 # the Qwen attention variants: per-head q/k RMSNorm, q/k/v bias
 # --------------------------------------------------------------------------
 VARIANT_SHAPES = {
@@ -315,53 +275,3 @@ def test_attention_variants(oracle_lib, name):
     o = oracle_rebuild(oracle_lib, wl, host_w, image)
     check_parity(wl, g, o, image)
     assert inv == {"free_changed": 0, "live_changed": 0, "tail_changed": 0, "written_bad": 0}
-
-
-# --------------------------------------------------------------------------
-# the full 8B benchmark workload: sampled layer-0 parity + invariants
-# --------------------------------------------------------------------------
-def test_full_config2_layer0_every_token_and_invariants(oracle_lib):
-    wl = W.config2()
-    say(f"config2 full: R={wl.num_requests} T={wl.total_tokens} NB={wl.num_blocks}")
-    model = Hn.device_model_random(wl.shape, seed=2)
-    arena = Hn.DeviceArena(wl)
-    arena.bind()
-    ws, nbytes = Hn.alloc_workspace(wl.shape, wl.num_requests, wl.total_tokens, wl.total_tokens, fill=0xFF)
-    kvr.kv_rebuild(model.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle,
-                   ws.data_ptr(), nbytes, Hn.stream_ptr())
-    torch.cuda.synchronize()
-    inv = arena.check_invariants()
-    say(f"  device invariants {inv}")
-    assert inv == {"free_changed": 0, "live_changed": 0, "tail_changed": 0, "written_bad": 0}
-    # layer-0 K/V of every token of the workload against the oracle's
-    # (layer 0 depends on the tokens and positions only)
-    req = np.repeat(np.arange(wl.num_requests), wl.lens)
-    pos = np.concatenate([np.arange(n) for n in wl.lens]).astype(np.int32)
-    toks = wl.tokens.astype(np.int32)
-    B = wl.block_size
-    blk_all = wl.block_tables[req, pos // B].astype(np.int64)
-    h0 = Hn.host_copy_layer0(model)
-    nkv, d = wl.shape.num_kv_heads, wl.shape.head_dim
-    num = {"K": np.zeros(nkv), "V": np.zeros(nkv)}
-    den = {"K": np.zeros(nkv), "V": np.zeros(nkv)}
-    same = {"K": 0, "V": 0}
-    step = 16384
-    for c0 in range(0, wl.total_tokens, step):
-        c1 = min(wl.total_tokens, c0 + step)
-        k_o, v_o = oracle_lib.layer0_kv(wl.shape, h0["embed"], h0["layer0"], toks[c0:c1], pos[c0:c1])
-        blk = torch.as_tensor(blk_all[c0:c1], device="cuda")
-        sl = torch.as_tensor(pos[c0:c1] % B, device="cuda")
-        for name, plane, o in (("K", 0, k_o), ("V", 1, v_o)):
-            g = arena.bits[0, plane][blk, sl].cpu().numpy().view(np.uint16).reshape(c1 - c0, -1)
-            gf = W.bf16_bits_to_f32(g).reshape(-1, nkv, d).astype(np.float64)
-            of = W.bf16_bits_to_f32(o).reshape(-1, nkv, d).astype(np.float64)
-            num[name] = np.maximum(num[name], np.abs(gf - of).max(axis=(0, 2)))
-            den[name] = np.maximum(den[name], np.abs(of).max(axis=(0, 2)))
-            same[name] += int(np.sum(g == o))
-        say(f"  layer-0 K/V of tokens {c0}..{c1 - 1} compared")
-    for name in ("K", "V"):
-        err = float(np.max(num[name] / den[name]))
-        exact = same[name] / (wl.total_tokens * nkv * d)
-        say(f"  layer-0 {name} over all {wl.total_tokens} tokens: normwise {err:.3e}, bit-exact {exact:.4f}")
-        assert err <= PU.TOL[W.BF16]
-    arena.release()
