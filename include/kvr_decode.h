@@ -32,7 +32,9 @@ uint64_t kv_decode_workspace_bytes(const kv_model_desc* desc, int32_t num_reques
  *   KV_EINVAL    null arrays, num_requests < 0, a position < 0
  *   KV_ERANGE    a token outside [0, vocab), a block entry outside [0, num_blocks)
  *   KV_ECAPACITY position / block_size >= max_blocks_per_req
- *   KV_EALIAS    one block listed twice among all requests' used entries */
+ *   KV_EALIAS    the block holding a request's position (the one the step
+ *                writes) listed anywhere else among the used entries of any
+ *                request; blocks the step only reads may be shared */
 kv_status kv_decode_check(const kv_model_desc* desc, int32_t block_size, int64_t num_blocks,
                           const int32_t* tokens, const int32_t* positions, int32_t num_requests,
                           const int32_t* block_tables, int32_t max_blocks_per_req);

@@ -36,8 +36,11 @@ typedef struct {
 
 /* Owner side: describe `bytes` bytes of device memory starting at `ptr` (any
  * pointer inside a device allocation of the calling process, with ptr+bytes
- * inside the same allocation).  KV_EINVAL for null arguments, KV_EDEVICE when
- * HIP does not know the pointer or cannot create a handle. */
+ * inside the same allocation).  A handle covers the whole allocation, and
+ * handles are limited to allocations below 2 GiB: larger ones are refused with
+ * KV_EINVAL (owners hold large weights and arenas as several allocations of
+ * less than 2 GiB each).  KV_EINVAL for null arguments, KV_EDEVICE when HIP
+ * does not know the pointer or cannot create a handle. */
 kv_status kv_ipc_export(const void* ptr, uint64_t bytes, kv_ipc_handle* out);
 
 /* Importer side: KV_OK when the process owner_pid exists, KV_ESTATE when it

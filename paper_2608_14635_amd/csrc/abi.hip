@@ -394,17 +394,31 @@ kv_status check_decode(const kv_model_desc* desc, int32_t B, int64_t NB, const i
                   positions[r], r, positions[r] / B, max_blocks);
     max_pos = std::max<int64_t>(max_pos, positions[r]);
   }
-  std::vector<uint8_t> seen((size_t)NB, 0);
-  for (int32_t r = 0; r < R; ++r) {
+  // The block holding a request's new position is written by the step: it
+  // may be listed only there, by that request.  Blocks the step only reads
+  // (full prefix blocks, for instance shared by several requests) may be
+  // listed any number of times.
+  for (int32_t r = 0; r < R; ++r)
     for (int32_t b = 0; b <= positions[r] / B; ++b) {
       const int32_t blk = tables[(int64_t)r * max_blocks + b];
       if (blk < 0 || blk >= NB)
         return fail(KV_ERANGE, "block_tables[%d][%d] = %d outside [0, %lld)", r, b, blk,
                     (long long)NB);
-      if (seen[blk]) return fail(KV_EALIAS, "block %d listed twice", blk);
-      seen[blk] = 1;
     }
+  std::vector<int32_t> writer((size_t)NB, -1);
+  for (int32_t r = 0; r < R; ++r) {
+    const int32_t blk = tables[(int64_t)r * max_blocks + positions[r] / B];
+    if (writer[blk] >= 0)
+      return fail(KV_EALIAS, "block %d holds the new positions of requests %d and %d", blk, writer[blk], r);
+    writer[blk] = r;
   }
+  for (int32_t r = 0; r < R; ++r)
+    for (int32_t b = 0; b <= positions[r] / B; ++b) {
+      const int32_t blk = tables[(int64_t)r * max_blocks + b];
+      if (writer[blk] >= 0 && (writer[blk] != r || b != positions[r] / B))
+        return fail(KV_EALIAS, "block %d, written by request %d's step, is also listed by request %d "
+                    "(entry %d)", blk, writer[blk], r, b);
+    }
   if (max_pos_out) *max_pos_out = max_pos;
   return KV_OK;
 }
@@ -1348,9 +1362,11 @@ VerifyLayout make_verify_layout(int32_t R, int64_t E) {
   return L;
 }
 
-kv_status verify_impl(kv_arena* arena, const int32_t* lens, int32_t R, const int32_t* tables,
-                      int32_t max_blocks, const uint64_t* committed, void* workspace,
-                      uint64_t ws_bytes, void* stream, uint64_t* digests, int32_t* intact) {
+// Host-side checks shared by the verification entry points; *E_out receives
+// the entry count.
+kv_status verify_check(kv_arena* arena, const int32_t* lens, int32_t R, const int32_t* tables,
+                       int32_t max_blocks, const uint64_t* committed, uint64_t* digests,
+                       int32_t* intact, int64_t* E_out) {
   if (!live_arena(arena)) return fail(KV_ESTATE, "unknown or released arena handle");
   if (R < 0) return fail(KV_EINVAL, "num_requests < 0");
   if (R > 0 && (!lens || !tables)) return fail(KV_EINVAL, "null lens or block tables");
@@ -1375,6 +1391,35 @@ kv_status verify_impl(kv_arena* arena, const int32_t* lens, int32_t R, const int
   if (E > 0x7fffffffLL) return fail(KV_EINVAL, "more than 2^31-1 blocks");
   if (E > 0 && !committed && !digests) return fail(KV_EINVAL, "null digest output");
   if (committed && R > 0 && !intact) return fail(KV_EINVAL, "null intact output");
+  *E_out = E;
+  return KV_OK;
+}
+
+DigestParams digest_params(const kv_arena* arena, const int2* entries, int64_t E,
+                           const uint64_t* committed, uint64_t* digests, uint8_t* match) {
+  const kv_model_desc& d = arena->desc;
+  const int64_t row = (int64_t)d.num_kv_heads * d.head_dim * elem_bytes(d.dtype);
+  DigestParams p;
+  p.arena = reinterpret_cast<const char*>(arena->base);
+  p.block_bytes = (int64_t)arena->block_size * row;
+  p.plane_bytes = arena->num_blocks * p.block_bytes;
+  p.row_bytes = (int32_t)row;
+  p.planes = 2 * d.num_layers;
+  p.entries = entries;
+  p.num_entries = E;
+  p.committed = committed;
+  p.digests = digests;
+  p.match = match;
+  return p;
+}
+
+kv_status verify_impl(kv_arena* arena, const int32_t* lens, int32_t R, const int32_t* tables,
+                      int32_t max_blocks, const uint64_t* committed, void* workspace,
+                      uint64_t ws_bytes, void* stream, uint64_t* digests, int32_t* intact) {
+  int64_t E = 0;
+  const kv_status cst = verify_check(arena, lens, R, tables, max_blocks, committed, digests, intact, &E);
+  if (cst != KV_OK) return cst;
+  const int32_t B = arena->block_size;
   if (R == 0) return ok();
   if (!workspace) return fail(KV_EINVAL, "null workspace");
   const VerifyLayout L = make_verify_layout(R, E);
@@ -1424,17 +1469,9 @@ kv_status verify_impl(kv_arena* arena, const int32_t* lens, int32_t R, const int
     }
     arena->staged_pending = true;
   }
-  DigestParams p;
-  p.arena = reinterpret_cast<const char*>(arena->base);
-  p.block_bytes = (int64_t)B * row;
-  p.plane_bytes = arena->num_blocks * p.block_bytes;
-  p.row_bytes = (int32_t)row;
-  p.planes = 2 * d.num_layers;
-  p.entries = reinterpret_cast<const int2*>(ws + L.entries);
-  p.num_entries = E;
-  p.committed = committed;
-  p.digests = digests ? digests : reinterpret_cast<uint64_t*>(ws + L.digests);
-  p.match = reinterpret_cast<uint8_t*>(ws + L.match);
+  const DigestParams p = digest_params(arena, reinterpret_cast<const int2*>(ws + L.entries), E, committed,
+                                      digests ? digests : reinterpret_cast<uint64_t*>(ws + L.digests),
+                                      reinterpret_cast<uint8_t*>(ws + L.match));
   launch_block_digest(p, s);
   if (committed)
     launch_leading_intact(reinterpret_cast<const int32_t*>(ws + L.offsets), R, p.match, intact, s);

@@ -28,6 +28,10 @@ std::map<void*, void*> g_opened;  // returned pointer -> mapped allocation base
 
 static_assert(sizeof(hipIpcMemHandle_t) <= 64, "IPC handle size");
 
+// Handles are limited to allocations below 2 GiB: opening a handle of a
+// larger allocation has been seen not to return.
+constexpr uint64_t IPC_MAX_ALLOCATION = 2ull << 30;
+
 }  // namespace
 
 extern "C" {
@@ -35,6 +39,9 @@ extern "C" {
 kv_status kv_ipc_export(const void* ptr, uint64_t bytes, kv_ipc_handle* out) {
   if (!ptr || !out || bytes == 0) return kvr_err::set(KV_EINVAL, "null pointer or zero size");
   std::memset(out, 0, sizeof *out);
+  if (bytes >= IPC_MAX_ALLOCATION)
+    return kvr_err::set(KV_EINVAL, "%llu bytes: handles are limited to allocations below 2 GiB",
+                        (unsigned long long)bytes);
   hipPointerAttribute_t attr;
   hipError_t e = hipPointerGetAttributes(&attr, ptr);
   if (e != hipSuccess || attr.type != hipMemoryTypeDevice) {
@@ -48,6 +55,9 @@ kv_status kv_ipc_export(const void* ptr, uint64_t bytes, kv_ipc_handle* out) {
     (void)hipGetLastError();
     return kvr_err::set(KV_EDEVICE, "no allocation range for the pointer: %s", hipGetErrorString(e));
   }
+  if (size >= IPC_MAX_ALLOCATION)
+    return kvr_err::set(KV_EINVAL, "the pointer lies in an allocation of %zu bytes: handles are limited "
+                        "to allocations below 2 GiB (export from a smaller allocation)", size);
   const uint64_t off = (uint64_t)(reinterpret_cast<const char*>(ptr) - reinterpret_cast<const char*>(base));
   if (off + bytes > size)
     return kvr_err::set(KV_EINVAL, "%llu bytes at offset %llu exceed the %zu-byte allocation",

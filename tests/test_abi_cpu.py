@@ -213,6 +213,7 @@ def test_decode_check_valid(L):
     ("needs_more_blocks", kvr.KV_ECAPACITY),
     ("alias_across_requests", kvr.KV_EALIAS),
     ("alias_within_request", kvr.KV_EALIAS),
+    ("two_writers_of_one_block", kvr.KV_EALIAS),
 ])
 def test_decode_check_errors(L, case, expect):
     shape, toks, pos, tables, B, NB = _decode_valid()
@@ -228,7 +229,22 @@ def test_decode_check_errors(L, case, expect):
         tables[2, 0] = tables[1, 0]
     elif case == "alias_within_request":
         tables[2, 2] = tables[2, 0]
+    elif case == "two_writers_of_one_block":
+        tables[1, 0] = tables[0, 0]
     assert kvr.kv_decode_check(shape, B, NB, toks, pos, tables) == expect
+
+
+def test_decode_check_allows_shared_read_only_blocks(L):
+    """Full prefix blocks the step only reads may be listed by several
+    requests (a shared system prompt), and twice by one request; the block
+    each request writes stays exclusive."""
+    shape, B, NB = W.TINY_BF16, 16, 12
+    pos = np.array([40, 47, 33], np.int32)
+    toks = np.array([1, 2, 3], np.int32)
+    tables = np.array([[0, 1, 2], [0, 1, 3], [0, 0, 4]], np.int32)
+    assert kvr.kv_decode_check(shape, B, NB, toks, pos, tables) == kvr.KV_OK
+    tables[2, 2] = 1  # request 2 would write block 1, which requests 0 and 1 read
+    assert kvr.kv_decode_check(shape, B, NB, toks, pos, tables) == kvr.KV_EALIAS
 
 
 def test_decode_check_ignores_unused_entries(L):
@@ -287,6 +303,15 @@ def test_ipc_open_refuses_before_device_access(L):
         kvr.kv_ipc_close(0x1000)
     assert e.value.status == kvr.KV_ESTATE
     assert L.kv_ipc_export(None, 16, None) == kvr.KV_EINVAL
+
+
+def test_ipc_export_refuses_two_gib_before_device_access(L):
+    """Handles are limited to allocations below 2 GiB; a range of 2 GiB or more
+    is refused on the host, before HIP is asked about the pointer."""
+    h = kvr.kv_ipc_handle()
+    assert L.kv_ipc_export(C.c_void_p(0x1000), 2 << 30, C.byref(h)) == kvr.KV_EINVAL
+    assert "2 GiB" in kvr.kv_last_error()
+    assert L.kv_ipc_export(C.c_void_p(0x1000), (2 << 30) + 4096, C.byref(h)) == kvr.KV_EINVAL
 
 
 def test_verify_workspace_bytes(L):

@@ -122,3 +122,16 @@ def test_rebuild_into_state_owned_by_another_process(oracle_lib, tmp_path, spec)
         if owner.poll() is None:
             owner.kill()
             owner.wait()
+
+
+def test_export_refuses_allocations_of_two_gib():
+    """A handle covers its whole allocation, and allocations of 2 GiB or more
+    are refused before any handle is created; a small allocation exports."""
+    big = torch.empty((2 << 30) + 4096, dtype=torch.uint8, device="cuda")
+    with pytest.raises(kvr.KvError) as e:
+        kvr.kv_ipc_export(big.data_ptr() + 4096, 4096)
+    assert e.value.status == kvr.KV_EINVAL and "2 GiB" in e.value.message
+    del big
+    torch.cuda.empty_cache()
+    small = torch.empty(1 << 19, dtype=torch.uint8, device="cuda")  # small pool: 2 MiB segments
+    assert len(kvr.kv_ipc_export(small.data_ptr(), 1 << 19)) > 0

@@ -88,8 +88,11 @@ def test_rebuild_from_matches_oracle(oracle_lib, name):
     before = arena.to_host().copy()
     gpu_from(model, wl, arena, piece(wl, starts, wl.lens), wl.lens, starts, wl.block_tables)
     got = arena.to_host()
-    # oracle on the GPU's own prefix contents: the same call
-    ora = before.copy()
+    # oracle: its own prefixes first, then the same call over them
+    ora = image.copy()
+    if starts.sum():
+        oracle_lib.rebuild(shape, host_w, piece(wl, zero, starts), starts, wl.block_tables, ora, B,
+                           wl.num_blocks)
     oracle_lib.rebuild_from(shape, host_w, piece(wl, starts, wl.lens), wl.lens, starts, wl.block_tables,
                             ora, B, wl.num_blocks)
     worst, rep = PU.compare(wl, got, ora, image)
@@ -150,7 +153,6 @@ def test_shared_prefix_blocks_in_one_call(oracle_lib):
     worst, rep = PU.compare(swl, got, ora, image)
     say(f"  vs oracle: worst {worst.max():.2e}; {rep}")
     assert rep["written_nonfinite"] == 0 and rep["worst"] <= PU.TOL[shape.dtype]
-    assert np.array_equal(got, got)  # noqa
     full = Hn.DeviceArena(wl, host_image=image)
     full.bind()
     gpu_full(model, wl, full, wl.tokens, wl.lens, wl.block_tables)
@@ -163,6 +165,70 @@ def test_shared_prefix_blocks_in_one_call(oracle_lib):
             assert np.array_equal(g, f), (r, p)
     arena.release()
     full.release()
+
+
+def test_decode_after_shared_prefix_rebuild(oracle_lib):
+    """Generation resumes over an arena whose requests share prefix blocks: one
+    decode step per request lists the shared blocks read-only and writes its
+    own last block; step K/V rows and logits match the oracle's step over the
+    oracle's arena, every greedy token is a maximum of the oracle's logits."""
+    shape, B, S = W.TINY_BF16, 16, 128
+    lens = [200, 150, 300]
+    wl = W.small_workload(shape, lens, block_size=B, seed=613, other_live_frac=0.25)
+    offs = wl.request_offsets()
+    toks = wl.tokens.copy()
+    for r in range(1, wl.num_requests):
+        toks[offs[r]:offs[r] + S] = toks[:S]
+    wl = dataclasses.replace(wl, tokens=toks)
+    shared = wl.block_tables.copy()
+    for r in range(1, wl.num_requests):
+        shared[r, :S // B] = wl.block_tables[0, :S // B]
+    starts = np.array([0] + [S] * (wl.num_requests - 1), np.int32)
+    model, host_w = model_for(shape, 614)
+    head = W.host_head_weights(shape, seed=615)
+    head_dev = Hn.device_head_from_host(shape, head)
+    image = W.host_arena(wl)
+    arena = Hn.DeviceArena(wl, host_image=image)
+    arena.bind()
+    say(f"[decode after shared prefix] lens {lens}, {S} shared tokens")
+    gpu_from(model, wl, arena, piece(wl, starts, wl.lens), wl.lens, starts, shared)
+    rebuilt = arena.to_host().copy()
+    ora = image.copy()
+    oracle_lib.rebuild_from(shape, host_w, piece(wl, starts, wl.lens), wl.lens, starts, shared, ora, B,
+                            wl.num_blocks)
+    # one step per request: its last token again at its last position
+    pos = (wl.lens - 1).astype(np.int32)
+    last = np.array([toks[offs[r + 1] - 1] for r in range(wl.num_requests)], np.int32)
+    assert kvr.kv_decode_check(shape, B, wl.num_blocks, last, pos, shared) == kvr.KV_OK
+    R = wl.num_requests
+    nbytes = kvr.kv_decode_workspace_bytes(shape, R, int(pos.max()) + 1)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    nxt = torch.zeros(R, dtype=torch.int32, device="cuda")
+    logits = torch.zeros((R, shape.vocab), dtype=torch.float32, device="cuda")
+    kvr.kv_decode_step(model.weights, head_dev["final_norm"].data_ptr(), head_dev["lm_head"].data_ptr(),
+                       last, pos, shared, arena.handle, ws.data_ptr(), nbytes, nxt.data_ptr(),
+                       logits.data_ptr(), Hn.stream_ptr())
+    torch.cuda.synchronize()
+    got = arena.to_host()
+    fh = oracle_lib.decode_step(shape, host_w, last, pos, shared, ora, B, wl.num_blocks)
+    z_o = oracle_lib.logits(shape, head, fh)
+    z_g = logits.cpu().numpy()
+    v = shape.num_layers, 2, wl.num_blocks, B, -1
+    blk, sl = shared[np.arange(R), pos // B], pos % B
+    g_rows = PU.to_float(got.reshape(v)[:, :, blk, sl], shape.dtype).astype(np.float64)
+    o_rows = PU.to_float(ora.reshape(v)[:, :, blk, sl], shape.dtype).astype(np.float64)
+    kv_err = float(np.max(np.abs(g_rows - o_rows)) / np.max(np.abs(o_rows)))
+    z_err = max(float(np.max(np.abs(z_g[r] - z_o[r])) / np.max(np.abs(z_o[r]))) for r in range(R))
+    tol = PU.TOL[shape.dtype]
+    say(f"  step K/V error {kv_err:.2e}, logits error {z_err:.2e}")
+    assert kv_err <= tol and z_err <= tol
+    for r, t in enumerate(nxt.cpu().numpy()):
+        z = z_o[r].astype(np.float64)
+        assert z[t] >= z.max() - tol * np.max(np.abs(z)), (r, int(t), int(np.argmax(z)))
+    # the shared prefix blocks are read, never written
+    pref = shared[0, :S // B]
+    assert np.array_equal(got.reshape(v)[:, :, pref], rebuilt.reshape(v)[:, :, pref])
+    arena.release()
 
 
 def test_partial_recovery_from_first_damaged_block(oracle_lib):
