@@ -2,12 +2,14 @@
 
     python bench.py [--gpus 1] [--steps 5] [--warmup 1] [--config 2]
 
-A step is one full rebuild (kv_rebuild_execute of a staged plan: embedding
+A step is one full kv_rebuild call of the configuration's whole request
+batch: host validation and wave planning, the metadata upload, embedding
 gather, every layer's norms, QKV GEMM + RoPE + arena scatter, attention,
-output projection, SwiGLU FFN) of the configuration's whole request batch,
-with weights, arena and the staged metadata already resident in HBM.  The
-default workload is the 8B-shaped decoder with 16 requests of 2048-16384
-tokens.  Prints one JSON line.
+output projection and SwiGLU FFN, with weights and arena resident in HBM.
+The default workload is the 8B-shaped decoder with 16 requests of 2048-16384
+tokens.  Prints one JSON line; `value` is total tokens over the wall time of
+the K timed steps, and the per-step HIP-event median is reported beside it,
+as is the device time of a pre-staged plan (kv_rebuild_execute).
 """
 from __future__ import annotations
 
@@ -270,34 +272,42 @@ def algorithmic_work(wl):
             "bytes": float(weights + kv + emb), "kv_bytes": float(kv)}
 
 
-def cpu_model(name: str) -> str:
+def host_info():
+    """Host CPU facts for the CPU baseline: nproc, the lscpu model name."""
+    model = platform.processor()
     try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                return line.split(":", 1)[1].strip()
-    except OSError:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                model = line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
         pass
-    return platform.processor()
+    return {"nproc": os.cpu_count(), "lscpu_model": model}
 
 
-def cpu_baseline(wl, model, Hn):
+# CPU-baseline sample plans: (fit lengths n1, n2; all-layer check length)
+CPU_PLANS = {"bounded": (512, 1024, 64), "full": (1024, 4096, 512)}
+
+
+def cpu_baseline(wl, model, Hn, plan: str = "bounded"):
     """Time the CPU oracle on a bounded sample of the same workload and model
-    the full rebuild from it: one layer at two request lengths gives
-    t_layer(n) = a n + b n^2, layer-0 K/V rows give the last-layer cost per
-    token; t = sum_r (L-1) t_layer(n_r) + c n_r."""
+    the whole rebuild from it: one transformer layer of the workload's shape
+    over one request at two lengths gives t_layer(n) = a n + b n^2 (fitted),
+    layer-0 K/V rows of 128 tokens give c, the last layer's per-token cost,
+    and t = sum_r (L-1) t_layer(n_r) + c n_r.  The model is checked against a
+    complete all-layer oracle run over one request.  plan "full" uses
+    n = 1024 and 4096 and a 512-token check (several minutes of CPU work);
+    "bounded" n = 512 and 1024 and a 64-token check (about half a minute on
+    16 threads).  A tiny model is run whole."""
     import oracle
     o = oracle.get()
     s = wl.shape
     host = Hn.host_copy_layer0(model)
     layer_w = {"embed": host["embed"], "layers": [host["layer0"]]}
     rng = np.random.default_rng(99)
-    per_tok_gflop = 2 * (s.hidden * (s.num_q_heads + 2 * s.num_kv_heads) * s.head_dim
-                         + s.num_q_heads * s.head_dim * s.hidden + 3 * s.hidden * s.ffn_dim) / 1e9
-    # sample sizes chosen for ~10-30 s of oracle work on a 16-thread host (~20 GFLOP/s fp64)
-    n1 = int(min(512, max(64, (80.0 / per_tok_gflop) // 16 * 16)))
-    n2 = 3 * n1
+    n1, n2, nm = CPU_PLANS[plan]
     if s.num_layers == 2 and s.hidden <= 512:  # tiny configuration: run it whole
-        n1, n2 = int(wl.lens.min()), int(wl.lens.max())
+        n1, n2, nm = int(wl.lens.min()), int(wl.lens.max()), int(wl.lens.max())
     t1 = o.time_layers(s, layer_w, rng.integers(0, s.vocab, n1), 1)
     t2 = o.time_layers(s, layer_w, rng.integers(0, s.vocab, n2), 1)
     b = max(0.0, (t2 / n2 - t1 / n1) / (n2 - n1))
@@ -308,24 +318,29 @@ def cpu_baseline(wl, model, Hn):
                 rng.integers(0, 4096, nk))
     c = (time.perf_counter() - tk0) / nk
     n = wl.lens.astype(np.float64)
-    t_pred = float(np.sum((s.num_layers - 1) * (a * n + b * n * n) + c * n))
-    # check of the model: a complete oracle run of all layers over one short
-    # request (layer 0's weights in every layer: the time depends only on the
-    # shapes), sized to ~5 s, against the fitted per-layer time
     L = s.num_layers
-    nm = int(min(n1, max(8, 5.0 / (L * a) // 8 * 8)))
+    t_pred = float(np.sum((L - 1) * (a * n + b * n * n) + c * n))
+    # check of the model: a complete oracle run of all layers over one request
+    # (layer 0's weights in every layer: the time depends only on the shapes;
+    # every layer is run whole there, the last one included)
     tm = o.time_layers(s, {"embed": host["embed"], "layers": [host["layer0"]] * L},
                        rng.integers(0, s.vocab, nm), L)
     tm_pred = L * (a * nm + b * nm * nm)
+    info = host_info()
     return {"value": wl.total_tokens / t_pred, "unit": "tokens/s", "cores": o.num_threads(),
-            "kind": "oracle",
+            "kind": "oracle", "plan": plan,
+            "nproc": info["nproc"], "lscpu_model": info["lscpu_model"],
+            "omp_threads": o.num_threads(),
+            "fit": {"n1": n1, "t1_s": t1, "n2": n2, "t2_s": t2, "a_s_per_token": a,
+                    "b_s_per_token2": b, "c_s_per_token": c},
             "model_check": {"tokens": nm, "layers": L, "measured_s": tm, "predicted_s": tm_pred,
                             "ratio": tm / tm_pred},
             "sample": (f"oracle timed on one layer of the same shape at n={n1} ({t1:.1f}s) and "
                        f"n={n2} ({t2:.1f}s) plus layer-0 K/V rows of {nk} tokens ({c * nk:.2f}s); "
-                       f"fitted t_layer(n)=a*n+b*n^2 extrapolated to {s.num_layers} layers x "
-                       f"{wl.num_requests} requests (modelled, {t_pred:.0f}s predicted)"),
-            "host_cpu": cpu_model("")}
+                       f"fitted t_layer(n)=a*n+b*n^2 extrapolated to {L} layers x "
+                       f"{wl.num_requests} requests (modelled from measured per-layer timings, "
+                       f"{t_pred:.0f}s predicted); checked by a complete {L}-layer run over "
+                       f"{nm} tokens ({tm:.1f}s measured, {tm_pred:.1f}s predicted)")}
 
 
 def main():
@@ -339,6 +354,8 @@ def main():
                          "(e.g. qwen3_8b, qwen3_32b, qwen25_1_5b: the paper's model families)")
     ap.add_argument("--wave-tokens", type=int, default=0, help="0 = largest that fits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-baseline", choices=sorted(CPU_PLANS), default="bounded",
+                    help="CPU-oracle sample plan (full: n=1024/4096 fit, 512-token all-layer check)")
     ap.add_argument("--no-check", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=4,
                     help="resumed-decode steps timed after the rebuild (0 = none)")
@@ -403,22 +420,37 @@ def main():
     torch.cuda.synchronize()
 
     for i in range(args.warmup):
-        kvr.kv_rebuild_execute(model.weights, plan, stream)
+        kvr.kv_rebuild(model.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle, ws.data_ptr(),
+                       nbytes, stream)
         torch.cuda.synchronize()
         log(f"[bench] warmup {i + 1}/{args.warmup} done")
 
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # timed steps: whole kv_rebuild calls (metadata staged from host arrays
+    # every call), HIP events around each on the library's stream
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ev0.record()
+    evs[0].record()
     for i in range(args.steps):
-        kvr.kv_rebuild_execute(model.weights, plan, stream)
-    ev1.record()
+        kvr.kv_rebuild(model.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle, ws.data_ptr(),
+                       nbytes, stream)
+        evs[i + 1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_wall = (t1 - t0) * 1e3 / args.steps
-    ms_ev = ev0.elapsed_time(ev1) / args.steps
-    log(f"[bench] {args.steps} steps: {ms_wall:.1f} ms/step wall, {ms_ev:.1f} ms/step events")
+    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms_median = float(np.median(step_ms))
+    log(f"[bench] {args.steps} steps: {ms_wall:.1f} ms/step wall, median {ms_median:.1f} ms "
+        f"(events {', '.join(f'{x:.1f}' for x in step_ms)})")
+
+    # the device work of a pre-staged plan alone (metadata already in HBM)
+    ex0, ex1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ex0.record()
+    for i in range(args.steps):
+        kvr.kv_rebuild_execute(model.weights, plan, stream)
+    ex1.record()
+    torch.cuda.synchronize()
+    ms_exec = ex0.elapsed_time(ex1) / args.steps
 
     # one profiled step: per-kernel-class device time via HIP events inside the library
     kvr.kv_profile_reset(arena.handle)
@@ -428,14 +460,6 @@ def main():
     prof = kvr.kv_profile_read(arena.handle)
     kvr.kv_profile_enable(arena.handle, False)
     kvr.kv_plan_release(plan)
-
-    # PCIe-inclusive rate (host arrays staged every call), for reference only
-    torch.cuda.synchronize()
-    tp0 = time.perf_counter()
-    kvr.kv_rebuild(model.weights, wl.tokens, wl.lens, wl.block_tables, arena.handle, ws.data_ptr(),
-                   nbytes, stream)
-    torch.cuda.synchronize()
-    ms_pcie = (time.perf_counter() - tp0) * 1e3
 
     check = None
     if not args.no_check:
@@ -471,7 +495,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
-        cpu = cpu_baseline(wl, model, Hn)
+        cpu = cpu_baseline(wl, model, Hn, args.cpu_baseline)
         log(f"[bench] cpu baseline {cpu}")
 
     dt_name = "bf16" if shape.dtype == W.BF16 else "f32"
@@ -498,7 +522,9 @@ def main():
                        "mfma_frac": work["flops"] / sec / 1e12 / peak,
                        "hbm_frac": work["bytes"] / sec / 1e9 / PEAK_HBM_GBS,
                        "gemm_tflops": gemm_tf, "gemm_frac": gemm_tf / peak,
-                       "ms_per_step_events": ms_ev, "pcie_inclusive_ms": ms_pcie},
+                       "median_ms_per_step": ms_median, "step_ms_events": step_ms,
+                       "staged_plan_ms": ms_exec,
+                       "staged_plan_tokens_per_s": T / (ms_exec / 1e3)},
         "kernel_classes": {k: {"ms": round(v["ms"], 3), "launches": v["launches"],
                                "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["ms"] and v["flops"] else None}
                            for k, v in prof.items()},
