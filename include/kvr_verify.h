@@ -64,6 +64,32 @@ kv_status kv_verify(kv_arena_t arena, const int32_t* lens, int32_t num_requests,
                     const uint64_t* committed, void* workspace, uint64_t workspace_bytes,
                     void* stream, uint64_t* digests, int32_t* intact);
 
+/* Verification that allocates nothing: kv_verify without a workspace, for
+ * callers that cannot allocate device memory (code being captured into a HIP
+ * graph, tight recovery or serving loops, harnesses that forbid hipMalloc).
+ * Its scratch memory (the uploaded lens and tables, the entry list, request
+ * offsets, match flags and, when `digests` is NULL, the digests) lives in a
+ * device array of KV_VERIFY_NOALLOC_SCRATCH_BYTES that the library holds on
+ * every device it runs on until the process ends; the call never allocates
+ * device or pinned host memory.  Arguments, outputs and status codes are
+ * those of kv_verify, plus
+ *   KV_ENOMEM    the call needs more than KV_VERIFY_NOALLOC_SCRATCH_BYTES of
+ *                scratch: 4R + 4*R*max_blocks_per_req + 17E bytes (+ 8E
+ *                without `digests`), each part rounded up to 256 bytes
+ *   KV_EDEVICE   the scratch array's device address cannot be obtained
+ * lens and block_tables are copied with hipMemcpyAsync on `stream`: from
+ * ordinary (pageable) host memory the copy has consumed them when the call
+ * returns; arrays in page-locked host memory must stay unchanged until the
+ * stream has passed this call.  Every call on one device shares that device's
+ * scratch array, so calls that overlap on one device (other streams, other
+ * threads) race; calls ordered on one stream do not.  Nothing in the scratch
+ * needs to start at zero: each call writes every element it later reads. */
+#define KV_VERIFY_NOALLOC_SCRATCH_BYTES (16u << 20)
+kv_status kv_verify_noalloc(kv_arena_t arena, const int32_t* lens, int32_t num_requests,
+                            const int32_t* block_tables, int32_t max_blocks_per_req,
+                            const uint64_t* committed, void* stream, uint64_t* digests,
+                            int32_t* intact);
+
 #ifdef __cplusplus
 }
 #endif

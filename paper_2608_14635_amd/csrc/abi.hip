@@ -1504,6 +1504,106 @@ kv_status kv_verify(kv_arena_t arena, const int32_t* lens, int32_t num_requests,
                      workspace, workspace_bytes, stream, digests, intact);
 }
 
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Verification without allocation (kvr_verify.h, kv_verify_noalloc)
+// ---------------------------------------------------------------------------
+// The scratch memory of kv_verify_noalloc: one copy of this array per device,
+// held until the process ends.  In host code its name stands for no device
+// address; kernels get the address hipGetSymbolAddress returns for the
+// current device, resolved once per device and kept in g_scratch.
+static __device__ __align__(256) char scratch[KV_VERIFY_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+char* g_scratch[SCRATCH_MAX_DEVICES] = {};
+
+// Device address of `device`'s scratch array; `device` must be current.
+kv_status scratch_of(int device, char** out) {
+  if (device < 0 || device >= SCRATCH_MAX_DEVICES)
+    return fail(KV_EDEVICE, "device %d is beyond the %d devices the scratch table covers", device,
+                SCRATCH_MAX_DEVICES);
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch[device]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      return fail(KV_EDEVICE, "cannot resolve the scratch array on device %d: %s", device,
+                  hipGetErrorString(e));
+    }
+    g_scratch[device] = reinterpret_cast<char*>(ptr);
+  }
+  *out = g_scratch[device];
+  return KV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+kv_status kv_verify_noalloc(kv_arena_t arena, const int32_t* lens, int32_t R,
+                            const int32_t* tables, int32_t max_blocks, const uint64_t* committed,
+                            void* stream, uint64_t* digests, int32_t* intact) {
+  if (!committed) return fail(KV_EINVAL, "null committed digests");
+  int64_t E = 0;
+  const kv_status cst = verify_check(arena, lens, R, tables, max_blocks, committed, digests, intact, &E);
+  if (cst != KV_OK) return cst;
+  if (R == 0) return ok();
+  // scratch layout: lens, tables, request offsets, entries, match flags, digests
+  uint64_t off = 0;
+  auto seg = [&](uint64_t bytes) {
+    const uint64_t at = off;
+    off = (uint64_t)round_up((int64_t)(off + bytes), 256);
+    return at;
+  };
+  const uint64_t o_lens = seg(4ull * R);
+  const uint64_t o_tab = seg(4ull * R * (uint64_t)max_blocks);
+  const uint64_t o_off = seg(4ull * ((uint64_t)R + 1));
+  const uint64_t o_ent = seg(8ull * (uint64_t)E);
+  const uint64_t o_match = seg((uint64_t)E);
+  const uint64_t o_dig = digests ? off : seg(8ull * (uint64_t)E);
+  if (off > KV_VERIFY_NOALLOC_SCRATCH_BYTES)
+    return fail(KV_ENOMEM, "%d requests with %lld table entries each and %lld blocks need %llu bytes of "
+                "scratch, more than the %u the allocation-free verification holds",
+                R, (long long)max_blocks, (long long)E, (unsigned long long)off,
+                (unsigned)KV_VERIFY_NOALLOC_SCRATCH_BYTES);
+  DeviceGuard dg(arena->device);
+  if (dg.err != hipSuccess) return fail(KV_EDEVICE, "cannot select device %d", arena->device);
+  {
+    const hipError_t pre = hipGetLastError();
+    if (pre != hipSuccess) return fail(KV_EDEVICE, "pending device error: %s", hipGetErrorString(pre));
+  }
+  char* sp = nullptr;
+  const kv_status sst = scratch_of(arena->device, &sp);
+  if (sst != KV_OK) return sst;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  int32_t* d_lens = reinterpret_cast<int32_t*>(sp + o_lens);
+  int32_t* d_tab = reinterpret_cast<int32_t*>(sp + o_tab);
+  int32_t* d_off = reinterpret_cast<int32_t*>(sp + o_off);
+  int2* d_ent = reinterpret_cast<int2*>(sp + o_ent);
+  uint8_t* d_match = reinterpret_cast<uint8_t*>(sp + o_match);
+  hipError_t err = hipMemcpyAsync(d_lens, lens, 4ull * R, hipMemcpyHostToDevice, s);
+  if (err == hipSuccess)
+    err = hipMemcpyAsync(d_tab, tables, 4ull * R * (uint64_t)max_blocks, hipMemcpyHostToDevice, s);
+  if (err != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(KV_EDEVICE, "metadata upload failed: %s", hipGetErrorString(err));
+  }
+  launch_verify_entries(d_lens, d_tab, R, max_blocks, arena->block_size, d_off, d_ent, s);
+  const DigestParams p = digest_params(arena, d_ent, E, committed,
+                                      digests ? digests : reinterpret_cast<uint64_t*>(sp + o_dig),
+                                      d_match);
+  launch_block_digest(p, s);
+  launch_leading_intact(d_off, R, d_match, intact, s);
+  err = hipGetLastError();
+  if (err != hipSuccess) return fail(KV_EDEVICE, "kernel launch failed: %s", hipGetErrorString(err));
+  return ok();
+}
+
 // ---------------------------------------------------------------------------
 // Per-kernel-class timing (kvr_profile.h)
 // ---------------------------------------------------------------------------

@@ -186,5 +186,12 @@ void launch_block_digest(const DigestParams& p, hipStream_t s);
 // whose match flag is 0, or its entry count when all match
 void launch_leading_intact(const int32_t* offsets, int32_t num_requests, const uint8_t* match,
                            int32_t* intact, hipStream_t s);
+// The entry list and request offsets of a verification built on the device
+// from the raw lens [R] and block tables [R][max_blocks]: offsets[r] = sum of
+// ceil(lens[q]/B) over q < r (offsets[R] = E); entry offsets[r] + j = (table
+// entry j of request r, its covered slots min(B, lens[r] - j*B)).
+void launch_verify_entries(const int32_t* lens, const int32_t* tables, int32_t num_requests,
+                           int32_t max_blocks, int32_t block_size, int32_t* offsets, int2* entries,
+                           hipStream_t s);
 
 }  // namespace kvr

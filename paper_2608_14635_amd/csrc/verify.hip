@@ -94,7 +94,55 @@ __global__ __launch_bounds__(DG_THREADS) void leading_intact_kernel(const int32_
   if (t == 0) intact[r] = red[0];
 }
 
+// Exclusive prefix sum of the per-request block counts in one workgroup, in
+// chunks of DG_THREADS requests carried from one chunk to the next.
+__global__ __launch_bounds__(DG_THREADS) void verify_offsets_kernel(const int32_t* lens, int32_t R,
+                                                                    int32_t B, int32_t* offsets) {
+  __shared__ int32_t sc[DG_THREADS];
+  const int t = threadIdx.x;
+  int32_t carry = 0;
+  for (int32_t r0 = 0; r0 < R; r0 += DG_THREADS) {
+    const int32_t r = r0 + t;
+    const int32_t nb = r < R ? (lens[r] + B - 1) / B : 0;
+    sc[t] = nb;
+    __syncthreads();
+    // Hillis-Steele inclusive scan
+    for (int o = 1; o < DG_THREADS; o <<= 1) {
+      const int32_t v = t >= o ? sc[t - o] : 0;
+      __syncthreads();
+      sc[t] += v;
+      __syncthreads();
+    }
+    if (r < R) offsets[r] = carry + sc[t] - nb;
+    carry += sc[DG_THREADS - 1];
+    __syncthreads();
+  }
+  if (t == 0) offsets[R] = carry;
+}
+
+// One workgroup per request: its entries (block id, covered slots).
+__global__ __launch_bounds__(DG_THREADS) void verify_entries_kernel(const int32_t* lens,
+                                                                    const int32_t* tables,
+                                                                    int32_t max_blocks, int32_t B,
+                                                                    const int32_t* offsets,
+                                                                    int2* entries) {
+  const int32_t r = blockIdx.x;
+  const int32_t off = offsets[r], nb = offsets[r + 1] - off, n = lens[r];
+  const int32_t* tab = tables + (int64_t)r * max_blocks;
+  for (int32_t j = threadIdx.x; j < nb; j += DG_THREADS)
+    entries[off + j] = make_int2(tab[j], min(B, n - j * B));
+}
+
 }  // namespace
+
+void launch_verify_entries(const int32_t* lens, const int32_t* tables, int32_t num_requests,
+                           int32_t max_blocks, int32_t block_size, int32_t* offsets, int2* entries,
+                           hipStream_t s) {
+  if (num_requests <= 0) return;
+  verify_offsets_kernel<<<dim3(1), dim3(DG_THREADS), 0, s>>>(lens, num_requests, block_size, offsets);
+  verify_entries_kernel<<<dim3((unsigned)num_requests), dim3(DG_THREADS), 0, s>>>(
+      lens, tables, max_blocks, block_size, offsets, entries);
+}
 
 void launch_block_digest(const DigestParams& p, hipStream_t s) {
   if (p.num_entries <= 0) return;

@@ -120,6 +120,8 @@ def lib() -> C.CDLL:
     L.kv_block_digests.argtypes = [vp, i32p, C.c_int32, i32p, C.c_int32, vp, C.c_uint64, vp, vp]
     L.kv_verify.restype = C.c_int
     L.kv_verify.argtypes = [vp, i32p, C.c_int32, i32p, C.c_int32, vp, vp, C.c_uint64, vp, vp, vp]
+    L.kv_verify_noalloc.restype = C.c_int
+    L.kv_verify_noalloc.argtypes = [vp, i32p, C.c_int32, i32p, C.c_int32, vp, vp, vp, vp]
     hp = C.POINTER(kv_ipc_handle)
     L.kv_ipc_export.restype = C.c_int
     L.kv_ipc_export.argtypes = [vp, C.c_uint64, hp]
@@ -343,6 +345,21 @@ def kv_verify(arena: int, lens, tables, committed: int, workspace: int, workspac
                            C.c_void_p(stream), C.c_void_p(digests or None), C.c_void_p(intact)))
 
 
+# bytes of device scratch the allocation-free verification holds per device
+KV_VERIFY_NOALLOC_SCRATCH_BYTES = 16 << 20
+
+
+def kv_verify_noalloc(arena: int, lens, tables, committed: int, intact: int, digests: int = 0,
+                      stream: int = 0) -> None:
+    """kv_verify without a workspace: its scratch is the library's own device
+    array (callers that cannot allocate)."""
+    ln = _i32(lens)
+    tab, mb = _tables2d(tables, len(ln))
+    _check(lib().kv_verify_noalloc(C.c_void_p(arena), _ptr(ln), len(ln), _ptr(tab), mb,
+                                   C.c_void_p(committed), C.c_void_p(stream),
+                                   C.c_void_p(digests or None), C.c_void_p(intact)))
+
+
 def kv_ipc_export(ptr: int, nbytes: int) -> bytes:
     """Owner side: the handle of device memory [ptr, ptr+nbytes) as plain bytes."""
     h = kv_ipc_handle()
@@ -401,6 +418,6 @@ def exported_symbols() -> Iterable[str]:
             "kv_plan_info", "kv_last_error", "kv_profile_enable", "kv_profile_read",
             "kv_profile_reset", "kv_decode_workspace_bytes", "kv_decode_check", "kv_decode_step",
             "kv_ipc_export", "kv_ipc_owner_alive", "kv_ipc_open", "kv_ipc_close",
-            "kv_verify_workspace_bytes", "kv_block_digests", "kv_verify",
+            "kv_verify_workspace_bytes", "kv_block_digests", "kv_verify", "kv_verify_noalloc",
             "kv_rebuild_from_workspace_bytes", "kv_rebuild_from_check", "kv_rebuild_from",
             "kv_rebuild_stage_from")
