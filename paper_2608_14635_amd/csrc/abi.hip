@@ -581,6 +581,8 @@ kv_status kv_arena_release(kv_arena_t a) {
   return ok();
 }
 
+}  // extern "C"
+
 namespace {
 
 kv_status stage_impl(kv_arena_t arena, const int32_t* tokens, const int32_t* lens,
@@ -775,6 +777,8 @@ kv_status stage_impl(kv_arena_t arena, const int32_t* tokens, const int32_t* len
 }
 
 }  // namespace
+
+extern "C" {
 
 kv_status kv_rebuild_stage(kv_arena_t arena, const int32_t* tokens, const int32_t* lens, int32_t R,
                            const int32_t* tables, int32_t max_blocks, void* workspace,
@@ -1336,6 +1340,8 @@ kv_status kv_decode_step(const kv_weights* w, const void* final_norm, const void
 // ---------------------------------------------------------------------------
 // Block commit digests and verification (kvr_verify.h)
 // ---------------------------------------------------------------------------
+}  // extern "C"
+
 namespace {
 
 // Workspace: the staged entry list (block, covered slots) and request offsets,
@@ -1481,6 +1487,8 @@ kv_status verify_impl(kv_arena* arena, const int32_t* lens, int32_t R, const int
 }
 
 }  // namespace
+
+extern "C" {
 
 uint64_t kv_verify_workspace_bytes(int32_t num_requests, int64_t num_entries) {
   if (num_requests < 0 || num_entries < 0) return 0;
