@@ -289,7 +289,37 @@ def host_info():
 CPU_PLANS = {"bounded": (512, 1024, 64), "full": (1024, 4096, 512)}
 
 
-def cpu_baseline(wl, model, Hn, plan: str = "bounded"):
+def _oracle_forward_time(o, s, embed, layer, tokens, L, log):
+    """Wall time of a complete L-layer oracle forward over one request, run one
+    layer per call: each layer's output rows, rounded to the model's dtype,
+    are the next call's input rows, and a line is printed per layer.  Layer
+    0's weights serve every layer (the time depends only on the shapes), and
+    every layer is run whole, the last one included."""
+    import dataclasses
+    from paper_2608_14635_amd import workloads as W
+    n = len(tokens)
+    one = dataclasses.replace(s, num_layers=1, vocab=n)
+    nb = (n + 15) // 16
+    tables = np.arange(nb, dtype=np.int32)[None, :]
+    ids = np.arange(n, dtype=np.int32)
+    lens = np.array([n], dtype=np.int32)
+    rows = np.ascontiguousarray(embed[np.asarray(tokens)])
+    arena = np.zeros(2 * nb * 16 * s.num_kv_heads * s.head_dim, dtype=embed.dtype)
+    total = 0.0
+    for l in range(L):
+        t0 = time.perf_counter()
+        fh = o.rebuild(one, {"embed": rows, "layers": [layer]}, ids, lens, tables, arena, 16, nb,
+                       final_hidden=True)
+        total += time.perf_counter() - t0
+        if s.dtype == W.BF16:
+            rows = W.f32_to_bf16_bits(fh.astype(np.float32))
+        else:
+            rows = np.ascontiguousarray(fh.astype(embed.dtype))
+        log(f"[bench] oracle check: layer {l + 1}/{L} over {n} tokens, {total:.1f}s so far")
+    return total
+
+
+def cpu_baseline(wl, model, Hn, plan: str = "bounded", log=lambda m: None):
     """Time the CPU oracle on a bounded sample of the same workload and model
     the whole rebuild from it: one transformer layer of the workload's shape
     over one request at two lengths gives t_layer(n) = a n + b n^2 (fitted),
@@ -324,7 +354,9 @@ def cpu_baseline(wl, model, Hn, plan: str = "bounded"):
     rng = np.random.default_rng(99)
     n1, n2, nm = CPU_PLANS[plan]
     t1 = o.time_layers(s, layer_w, rng.integers(0, s.vocab, n1), 1)
+    log(f"[bench] oracle: one layer over {n1} tokens in {t1:.1f}s")
     t2 = o.time_layers(s, layer_w, rng.integers(0, s.vocab, n2), 1)
+    log(f"[bench] oracle: one layer over {n2} tokens in {t2:.1f}s")
     b = max(0.0, (t2 / n2 - t1 / n1) / (n2 - n1))
     a = max(1e-12, t1 / n1 - b * n1)
     nk = 128
@@ -332,14 +364,12 @@ def cpu_baseline(wl, model, Hn, plan: str = "bounded"):
     o.layer0_kv(s, host["embed"], host["layer0"], rng.integers(0, s.vocab, nk),
                 rng.integers(0, 4096, nk))
     c = (time.perf_counter() - tk0) / nk
+    log(f"[bench] oracle: layer-0 K/V rows of {nk} tokens in {c * nk:.2f}s")
     n = wl.lens.astype(np.float64)
     L = s.num_layers
     t_pred = float(np.sum((L - 1) * (a * n + b * n * n) + c * n))
-    # check of the model: a complete oracle run of all layers over one request
-    # (layer 0's weights in every layer: the time depends only on the shapes;
-    # every layer is run whole there, the last one included)
-    tm = o.time_layers(s, {"embed": host["embed"], "layers": [host["layer0"]] * L},
-                       rng.integers(0, s.vocab, nm), L)
+    # check of the model: a complete oracle forward of all layers over one request
+    tm = _oracle_forward_time(o, s, host["embed"], host["layer0"], rng.integers(0, s.vocab, nm), L, log)
     tm_pred = L * (a * nm + b * nm * nm)
     return {"value": wl.total_tokens / t_pred, "unit": "tokens/s", "cores": o.num_threads(),
             "kind": "oracle", "plan": plan,
@@ -353,7 +383,7 @@ def cpu_baseline(wl, model, Hn, plan: str = "bounded"):
                        f"n={n2} ({t2:.1f}s) plus layer-0 K/V rows of {nk} tokens ({c * nk:.2f}s); "
                        f"fitted t_layer(n)=a*n+b*n^2 extrapolated to {L} layers x "
                        f"{wl.num_requests} requests (modelled from measured per-layer timings, "
-                       f"{t_pred:.0f}s predicted); checked by a complete {L}-layer run over "
+                       f"{t_pred:.0f}s predicted); checked by a complete {L}-layer forward, one layer per call, over "
                        f"{nm} tokens ({tm:.1f}s measured, {tm_pred:.1f}s predicted)")}
 
 
@@ -509,7 +539,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
-        cpu = cpu_baseline(wl, model, Hn, args.cpu_baseline)
+        cpu = cpu_baseline(wl, model, Hn, args.cpu_baseline, log)
         log(f"[bench] cpu baseline {cpu}")
 
     dt_name = "bf16" if shape.dtype == W.BF16 else "f32"

@@ -275,3 +275,24 @@ def test_attention_variants(oracle_lib, name):
     o = oracle_rebuild(oracle_lib, wl, host_w, image)
     check_parity(wl, g, o, image)
     assert inv == {"free_changed": 0, "live_changed": 0, "tail_changed": 0, "written_bad": 0}
+
+
+def test_attention_with_scores_spread_over_thousands(oracle_lib):
+    """Scores spread over thousands of units (layer-0 Wq and Wk scaled by 100):
+    the running maxima rise tile after tile by far more than the rescale
+    slack, so the rescale factors span the whole exponent range and many
+    underflow to zero, and the softmax is nearly one-hot.  The rebuild
+    matches the oracle and every value is finite."""
+    shape = W.TINY_BF16.with_layers(2)
+    wl = W.small_workload(shape, [300, 1000, 17], seed=471, other_live_frac=0.2)
+    host_w = W.host_weights(shape, seed=472, gain_std=0.1)
+    for key in ("wq", "wk"):
+        w = W.bf16_bits_to_f32(host_w["layers"][0][key]) * np.float32(100.0)
+        host_w["layers"][0][key] = W.f32_to_bf16_bits(w)
+    say(f"attention with scores spread over thousands: lens={wl.lens.tolist()}")
+    image = W.host_arena(wl)
+    model = Hn.device_model_from_host(shape, host_w)
+    g, arena = gpu_rebuild(wl, model, host_image=image)
+    arena.release()
+    o = oracle_rebuild(oracle_lib, wl, host_w, image)
+    check_parity(wl, g, o, image)
