@@ -286,7 +286,7 @@ def host_info():
 
 
 # CPU-baseline sample plans: (fit lengths n1, n2; all-layer check length)
-CPU_PLANS = {"bounded": (512, 1024, 64), "full": (1024, 4096, 512)}
+CPU_PLANS = {"bounded": (1024, 4096, 64), "full": (1024, 4096, 512)}
 
 
 def _oracle_forward_time(o, s, embed, layer, tokens, L, log):
@@ -325,10 +325,12 @@ def cpu_baseline(wl, model, Hn, plan: str = "bounded", log=lambda m: None):
     over one request at two lengths gives t_layer(n) = a n + b n^2 (fitted),
     layer-0 K/V rows of 128 tokens give c, the last layer's per-token cost,
     and t = sum_r (L-1) t_layer(n_r) + c n_r.  The model is checked against a
-    complete all-layer oracle run over one request.  plan "full" uses
-    n = 1024 and 4096 and a 512-token check (several minutes of CPU work);
-    "bounded" n = 512 and 1024 and a 64-token check (about half a minute on
-    16 threads).  A tiny model's whole rebuild is timed instead (median of 5)."""
+    complete all-layer oracle run over one request.  Both plans fit at
+    n = 1024 and 4096 (about a minute of CPU work for the 8B shape on 16
+    threads: shorter requests make the quadratic attention term too small for
+    requests of up to 16K tokens); "full" checks on 512 tokens (three more
+    minutes), "bounded" on 64.  A tiny model's whole rebuild is timed instead
+    (median of 5)."""
     import oracle
     from paper_2608_14635_amd import workloads as W
     o = oracle.get()
@@ -399,7 +401,7 @@ def main():
     ap.add_argument("--wave-tokens", type=int, default=0, help="0 = largest that fits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-baseline", choices=sorted(CPU_PLANS), default="bounded",
-                    help="CPU-oracle sample plan (full: n=1024/4096 fit, 512-token all-layer check)")
+                    help="CPU-oracle sample plan (n=1024/4096 fit; all-layer check on 64 tokens, full: 512)")
     ap.add_argument("--no-check", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=4,
                     help="resumed-decode steps timed after the rebuild (0 = none)")

@@ -37,6 +37,7 @@ constexpr int VTILE = D * KB * 2;            // 16 KB: 128 V^T rows of 128 B
 constexpr int STAGE = KTILE + VTILE;
 constexpr int NSTAGE = 3;
 constexpr float RESCALE_SLACK = 8.0f;        // see the online softmax below
+constexpr int READ_AHEAD = 4;                // LDS fragment reads in flight ahead of the MFMAs
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -46,6 +47,20 @@ __device__ __forceinline__ int ksig(int r) { return (r & ~12) | ((r & 4) << 1) |
 // Both make the MFMA operand reads (32 consecutive rows, one unit) conflict-free
 // for 8- or 16-lane LDS read phases.
 __device__ __forceinline__ int vsw(int d) { return (d & 7) ^ ((d >> 3) & 1); }
+
+// v_permlane32_swap of a register with itself: one result holds the lower
+// half's values in both halves, the other the upper half's, so a symmetric
+// combination of the two is the lane's value combined with lane (lane ^ 32)'s
+__device__ __forceinline__ float max_with_other_half(float x) {
+  const unsigned u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_with_other_half(float x) {
+  const unsigned u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 #define KVR_WAIT_VMCNT(n) \
   __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (((n) >> 4) << 14) | (0x7 << 4) | (0xF << 8))
@@ -171,15 +186,15 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
               *reinterpret_cast<const bf16x8*>(krow + (((2 * ks + half) ^ kslot0) << 4));
           s[k2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[k2], 0, 0, 0);
         }
-      // K fragment reads run four ahead of the MFMAs that consume them
+      // K fragment reads run READ_AHEAD ahead of the MFMAs that consume them
 #pragma unroll
-      for (int q = 0; q < 4; ++q) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      for (int q = 0; q < READ_AHEAD; ++q) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
 #pragma unroll
-      for (int q = 0; q < 12; ++q) {
+      for (int q = 0; q < 16 - READ_AHEAD; ++q) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, READ_AHEAD, 0);
       // ---- mask on diagonal tiles, online softmax ----
       // The running max m_run lives in the log2 domain (scores times
       // log2(e)/sqrt(d)); the scale is folded into the FMA that forms each
@@ -199,12 +214,19 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
             if (kc > lim) s[k2][r] = -INFINITY;
           }
       }
-      float mx = s[0][0];
+      // the lane's max as four independent chains (short dependency depth),
+      // then the other half of its query column's keys via a lane swap
+      // (IEEE maximum: v_maximum3_f32, with no quieting of the MFMA results)
+      float mq[4];
 #pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2)
+      for (int j = 0; j < 4; ++j) {
+        mq[j] = s[0][j];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[k2][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * scale_log2;
+        for (int i = 1; i < 8; ++i) mq[j] = __builtin_elementwise_maximum(mq[j], s[i >> 2][4 * (i & 3) + j]);
+      }
+      float mx = __builtin_elementwise_maximum(__builtin_elementwise_maximum(mq[0], mq[1]),
+                                               __builtin_elementwise_maximum(mq[2], mq[3]));
+      mx = max_with_other_half(mx) * scale_log2;
       // The reference max used for the exponents may lag the true running
       // max by up to RESCALE_SLACK (log2 units): P then reaches at most
       // 2^RESCALE_SLACK, which the fp32 sums and the final division by l
@@ -252,21 +274,21 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
                                                               (((2 * c + half) ^ vsw_l[t]) << 4));
           acc_o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[c], acc_o[t], 0, 0, 0);
         }
-      // V^T fragment reads run four ahead of their MFMAs
+      // V^T fragment reads run READ_AHEAD ahead of their MFMAs
 #pragma unroll
-      for (int q = 0; q < 4; ++q) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      for (int q = 0; q < READ_AHEAD; ++q) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
 #pragma unroll
-      for (int q = 0; q < 12; ++q) {
+      for (int q = 0; q < 16 - READ_AHEAD; ++q) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, READ_AHEAD, 0);
     }
   }
   KVR_WAIT_VMCNT(0);  // trailing refetches complete before the workgroup retires
 
   if (!wave_active) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float l_tot = sum_with_other_half(l_run);
   const float inv = 1.0f / l_tot;
   const int q_local = qsub * 32 + col;
   if (q_local >= q_len) return;
