@@ -9,7 +9,8 @@
 //            arena slots, and V^T columns for the attention kernel;
 //   RESID  : X += acc on the fp32 residual stream;
 //   STORE  : X = acc (the transposed logits of the decode step's LM head);
-//   SWIGLU : h = silu(gate) * up from the two column halves of the tile.
+//   SWIGLU : h = silu(gate) * up from the two column halves of the tile (the
+//            split-K path; the one-pass bf16 GEMM forms h from its accumulators).
 #pragma once
 #include "common.h"
 #include "launch.h"

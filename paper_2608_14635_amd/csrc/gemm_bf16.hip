@@ -90,7 +90,8 @@ typedef __attribute__((address_space(3))) void lds_void;
 //      offset (rows past M are clamped to row M-1, their results dropped).
 //   B: rows 0..127 and 128..255 of the tile each sit in one weight matrix
 //      (the QKV split points are multiples of 256 and a gate/up tile is 128
-//      gate rows then 128 up rows); the block's row offset is scalar.
+//      gate rows then 128 up rows; the one-pass gate/up product takes them in
+//      quarters instead, see issue_slot); the block's row offset is scalar.
 struct Loader {
   const void* a;            // tile row 0 of A
   const void* b_lo;         // tile row 0 of B
@@ -106,9 +107,13 @@ constexpr int BUF_WORD3 = 0x00020000;  // gfx9 buffer descriptor: 32-bit data fo
 
 // Issue loads q in [Q0, Q1) of one ring slot holding operand B (IS_B) or A at
 // K tile kt, into ring position slot % NSLOT (wave `wid` fills blocks wid,
-// wid+WAVES, ...).
-template <bool IS_B, int Q0, int Q1>
+// wid+WAVES, ...).  GU: the B tile of the fused gate/up product holds its
+// 128 gate rows and 128 up rows in quarters of 64 (gate j0.., up j0..,
+// gate j0+64.., up j0+64..), so that each wave column's accumulators hold
+// the gate and the up values of the same 64 outputs.
+template <bool IS_B, int Q0, int Q1, bool GU>
 __device__ __forceinline__ void issue_slot(char* smem, const Loader& L, int kt, int slot, int wid) {
+  static_assert(!GU || WAVES == 4, "the gate/up quarter layout assumes 8 B blocks per wave");
   const int kbytes = L.k_base_bytes + kt * BK * 2;
   char* st = smem + (slot % Ring::NSLOT) * Ring::HALF;
 #pragma unroll
@@ -116,8 +121,10 @@ __device__ __forceinline__ void issue_slot(char* smem, const Loader& L, int kt, 
     lds_void* dst = (lds_void*)(st + (wid + WAVES * q) * 1024);
     if constexpr (IS_B) {
       constexpr int HB = Ring::BLOCKS / 2;  // blocks per 128-row half
-      const bool hi = q >= Ring::LOADS / 2;
-      const int soff = kbytes + (wid + WAVES * q - (hi ? HB : 0)) * L.b_block_bytes;
+      // tile block wid + 4q sits in quarter q/2; gate quarters are 0 and 2
+      const bool hi = GU ? ((q >> 1) & 1) != 0 : q >= Ring::LOADS / 2;
+      const int blk = GU ? (q >> 2) * 8 + wid + 4 * (q & 1) : wid + WAVES * q - (hi ? HB : 0);
+      const int soff = kbytes + blk * L.b_block_bytes;
       const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(hi ? L.b_hi : L.b_lo), 0,
                                                           L.b_bytes, BUF_WORD3);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, L.b_voff, soff, 0, 0);
@@ -129,22 +136,22 @@ __device__ __forceinline__ void issue_slot(char* smem, const Loader& L, int kt, 
   }
 }
 
-template <bool IS_B>
+template <bool IS_B, bool GU>
 __device__ __forceinline__ void issue_whole(char* smem, const Loader& L, int kt, int slot, int wid) {
-  issue_slot<IS_B, 0, Ring::LOADS>(smem, L, kt, slot, wid);
+  issue_slot<IS_B, 0, Ring::LOADS, GU>(smem, L, kt, slot, wid);
 }
 
 // Share of k-step KS in the load issue of a K tile's two slots s0 and s0+1:
 // the first half of the k-steps issues slot s0, the second half slot s0+1.
-template <int KS, bool S0_IS_B>
+template <int KS, bool S0_IS_B, bool GU>
 __device__ __forceinline__ void issue_step(char* smem, const Loader& L, int k_s0, int k_s1, int s0,
                                            int wid) {
   constexpr int SPS = (BK / 16) / 2;  // k-steps per slot
   constexpr int QS = Ring::LOADS / SPS;
   if constexpr (KS < SPS)
-    issue_slot<S0_IS_B, (KS % SPS) * QS, (KS % SPS + 1) * QS>(smem, L, k_s0, s0, wid);
+    issue_slot<S0_IS_B, (KS % SPS) * QS, (KS % SPS + 1) * QS, GU>(smem, L, k_s0, s0, wid);
   else
-    issue_slot<!S0_IS_B, (KS % SPS) * QS, (KS % SPS + 1) * QS>(smem, L, k_s1, s0 + 1, wid);
+    issue_slot<!S0_IS_B, (KS % SPS) * QS, (KS % SPS + 1) * QS, GU>(smem, L, k_s1, s0 + 1, wid);
 }
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding)
@@ -157,6 +164,7 @@ constexpr int SG_MFMA = 0x008, SG_VMEM = 0x010, SG_DS_READ = 0x100;
 template <int EPI>
 __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m, int tiles_n) {
   constexpr int SMEM = Ring::BYTES > EPI_BYTES ? Ring::BYTES : EPI_BYTES;
+  constexpr bool GU = EPI == EPI_SWIGLU;  // gate/up B tile in quarters, SwiGLU in registers
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   // ---- split-K pass: consecutive workgroups share a tile, one K range each ----
@@ -215,9 +223,9 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
 #pragma unroll
   for (int s = 0; s < Ring::NSLOT - 2; ++s) {
     if (s & 1)
-      issue_whole<true>(smem, L, min(s >> 1, KT - 1), s, wave);
+      issue_whole<true, GU>(smem, L, min(s >> 1, KT - 1), s, wave);
     else
-      issue_whole<false>(smem, L, min(s >> 1, KT - 1), s, wave);
+      issue_whole<false, GU>(smem, L, min(s >> 1, KT - 1), s, wave);
   }
 
   // fragment reads: lane%32 picks the row, lane/32 the 8-wide k half
@@ -297,10 +305,10 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
         for (int i = 1; i < FI; ++i)
           af[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(sta + a_base[i] + ((cn ^ a_sw[i]) << 4));
       }
-      if (ks == 0) issue_step<0, S0_IS_B>(smem, L, k_s0, k_s1, s0, wave);
-      if (ks == 1) issue_step<1, S0_IS_B>(smem, L, k_s0, k_s1, s0, wave);
-      if (ks == 2) issue_step<2, S0_IS_B>(smem, L, k_s0, k_s1, s0, wave);
-      if (ks == 3) issue_step<3, S0_IS_B>(smem, L, k_s0, k_s1, s0, wave);
+      if (ks == 0) issue_step<0, S0_IS_B, GU>(smem, L, k_s0, k_s1, s0, wave);
+      if (ks == 1) issue_step<1, S0_IS_B, GU>(smem, L, k_s0, k_s1, s0, wave);
+      if (ks == 2) issue_step<2, S0_IS_B, GU>(smem, L, k_s0, k_s1, s0, wave);
+      if (ks == 3) issue_step<3, S0_IS_B, GU>(smem, L, k_s0, k_s1, s0, wave);
       const int m_end = ks + 1 < KS ? MF : PBAR;
 #pragma unroll
       for (int m = 0; m < m_end; ++m)
@@ -356,6 +364,43 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmParams p, int tiles_m
     }
   }
   KVR_WAIT_VMCNT(0);  // the trailing refetches land before the ring becomes the C tile
+
+  if constexpr (GU) {
+    // ---- SwiGLU from the accumulators: tile columns wn*128 + [0, 64) hold
+    // the gate and wn*128 + [64, 128) the up values of outputs
+    // j0 + wn*64 + [0, 64) (the quarter layout of the B tile); a lane has one
+    // output column of each 32-column tile and 16 of its rows ----
+    const int j0 = tile_n * (BN / 2);
+    const int oc0 = j0 + wn * 64 + (lane & 31);
+    const int row0 = m0 + wm * 128 + 4 * (lane >> 5);
+    bf16_t* hf = reinterpret_cast<bf16_t*>(p.epi.hf) + (int64_t)row0 * p.epi.ldh + oc0;
+    if (m0 + BM <= p.M && j0 + BN / 2 <= p.epi.ffn) {
+      // (two-byte stores: each instruction writes 64-byte row segments, whose
+      // other halves the same wave writes next; a transpose within quads of
+      // lanes for 8-byte stores measured 1 % slower)
+#pragma unroll
+      for (int i = 0; i < FI; ++i)
+#pragma unroll
+        for (int j = 0; j < FJ / 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int dr = i * 32 + 8 * (r >> 2) + (r & 3);
+            hf[(int64_t)dr * p.epi.ldh + j * 32] = f2bf(silu(acc[i][j][r]) * acc[i][j + 2][r]);
+          }
+    } else {
+#pragma unroll
+      for (int i = 0; i < FI; ++i)
+#pragma unroll
+        for (int j = 0; j < FJ / 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int dr = i * 32 + 8 * (r >> 2) + (r & 3);
+            if (row0 + dr < p.M && oc0 + j * 32 < p.epi.ffn)
+              hf[(int64_t)dr * p.epi.ldh + j * 32] = f2bf(silu(acc[i][j][r]) * acc[i][j + 2][r]);
+          }
+    }
+    return;
+  }
 
   // ---- epilogue: two passes of 128 rows through LDS ----
   __syncthreads();  // all waves are done with the ring before it becomes the C tile
