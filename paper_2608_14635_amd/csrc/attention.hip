@@ -4,8 +4,9 @@
 // group x QW blocks of 32 queries of one request (HW * QW = 8), so every K/V
 // tile staged in LDS feeds 8 waves.  Key tiles of 64 keys stream into a
 // 3-stage LDS ring with buffer_load_dwordx4 ... lds (two tiles in flight): K rows
-// from a contiguous per-head copy of the stored K, V from the V^T copy, both
-// written by the QKV epilogue with the values sent to the arena.  Scores are
+// from a contiguous per-head copy of the stored K, V from the V^T copy (one
+// contiguous 16 KB block per key tile), both written by the QKV epilogue with
+// the values sent to the arena.  Scores are
 // computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: a lane owns
 // one query column and 32 of the tile's keys in registers, so the online
 // softmax statistics are per-lane scalars completed by one cross-half
@@ -37,6 +38,7 @@ constexpr int VTILE = D * KB * 2;            // 16 KB: 128 V^T rows of 128 B
 constexpr int STAGE = KTILE + VTILE;
 constexpr int NSTAGE = 3;
 constexpr float RESCALE_SLACK = 8.0f;        // see the online softmax below
+static_assert(KB == VT_KEYS, "a key tile is one tile of the V^T copy");
 constexpr int READ_AHEAD = 4;                // LDS fragment reads in flight ahead of the MFMAs
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -71,8 +73,8 @@ constexpr int BUF_WORD3 = 0x00020000;  // gfx9 buffer descriptor: 32-bit data fo
 // starting at row kbase into ring stage `stage`.  Buffer loads with the LDS
 // bit are counted by vmcnt only, so the fragment reads from LDS keep exact
 // lgkm counts (global_load_lds would force lgkmcnt(0) before every MFMA).
-// k_voff / v_voff: this lane's byte offsets within the head's K copy / V^T
-// rows for key 0; the tile's key offset is scalar.
+// k_voff / v_voff: this lane's byte offsets within the head's K copy at key
+// 0 / within a V^T key tile; the tile's offset is scalar.
 __device__ __forceinline__ void issue_kv(char* smem, const bf16_t* Kc, const bf16_t* Vt,
                                          int head_bytes, int kbase, int stage, int wid,
                                          const int* k_voff, const int* v_voff) {
@@ -85,7 +87,7 @@ __device__ __forceinline__ void issue_kv(char* smem, const bf16_t* Kc, const bf1
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(st + qk * 1024), 16, k_voff[i],
                                              kbase * D * 2, 0, 0);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(st + KTILE + qk * 1024), 16, v_voff[i],
-                                             kbase * 2, 0, 0);
+                                             kbase * D * 2, 0, 0);  // key tile kbase / 64: 16 KB
   }
 }
 
@@ -138,7 +140,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     // key ksig(lr) lands there; unit (lane&15)^(lr&15) of it fills this lane's slot
     k_voff[i] = (ksig(lr) * D + ((lane & 15) ^ (lr & 15)) * 8) * 2;
     const int dv = 8 * qk + (lane >> 3);
-    v_voff[i] = (dv * (int)p.ldvt + ((lane & 7) ^ vsw(dv)) * 8) * 2;
+    v_voff[i] = (dv * VT_KEYS + ((lane & 7) ^ vsw(dv)) * 8) * 2;  // within the key tile
   }
 
   f32x16 acc_o[D / 32];
@@ -380,7 +382,7 @@ __global__ __launch_bounds__(256) void prefix_gather_kernel(const int2* segs, co
     for (int it = tid; it < z * (D / 8); it += 256)
       *reinterpret_cast<uint4*>(kc + ((int64_t)h * ldvt + kr0 + it / (D / 8)) * D + (it % (D / 8)) * 8) = zero;
     for (int it = tid; it < D * (z / 8); it += 256)
-      *reinterpret_cast<uint4*>(vt + ((int64_t)h * D + it % D) * ldvt + kr0 + (it / D) * 8) = zero;
+      *reinterpret_cast<uint4*>(vt + vt_offset(h * D + it % D, kr0 + (it / D) * 8, ldvt, D)) = zero;
     return;
   }
   const int64_t row_elems = (int64_t)nkv * D;
@@ -398,7 +400,7 @@ __global__ __launch_bounds__(256) void prefix_gather_kernel(const int2* segs, co
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       w[i] = (uint32_t)sv[(k8 + 2 * i) * GP + e] | ((uint32_t)sv[(k8 + 2 * i + 1) * GP + e] << 16);
-    *reinterpret_cast<uint4*>(vt + ((int64_t)h * D + e) * ldvt + kr0 + k8) = make_uint4(w[0], w[1], w[2], w[3]);
+    *reinterpret_cast<uint4*>(vt + vt_offset(h * D + e, kr0 + k8, ldvt, D)) = make_uint4(w[0], w[1], w[2], w[3]);
   }
 }
 

@@ -163,9 +163,9 @@ __device__ __forceinline__ void epi_qkv_v_full(float* sC, int ldc, int rows, int
   }
   if (e.vt == nullptr) return;
   __syncthreads();
-  // V^T[col][krow(m)]: 8 consecutive rows of one column per item (their key
-  // rows are consecutive: a request's rows start on a multiple of 8, and so
-  // do its suffix key rows); padding rows get zeros
+  // V^T (col, krow(m)): 8 consecutive rows of one column per item (their key
+  // rows are consecutive and inside one key tile: a request's rows start on a
+  // multiple of 8, and so do its suffix key rows); padding rows get zeros
   for (int it = tid; it < BN * (rows / 8); it += NT) {
     const int c = it % BN, rc = it / BN;
     const float* src = sC + (int64_t)(rc * 8) * ldc;
@@ -173,7 +173,7 @@ __device__ __forceinline__ void epi_qkv_v_full(float* sC, int ldc, int rows, int
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = src[(int64_t)i * ldc + BN] != 0.0f ? 0.0f : src[(int64_t)i * ldc + c];
     const int64_t kr0 = __float_as_int(src[BN + 1]);
-    store8(reinterpret_cast<T*>(e.vt) + (int64_t)(vbase + c) * e.ldvt + kr0, v);
+    store8(reinterpret_cast<T*>(e.vt) + vt_offset(vbase + c, kr0, e.ldvt, e.d), v);
   }
 }
 
@@ -334,10 +334,10 @@ __device__ __forceinline__ void epi_qkv(float* sC, int ldc, int rows, int m_base
       store8(dst, v);
     }
     if (e.vt != nullptr) {
-      // V^T[col][krow(m)]: 8 consecutive rows of one column per item (their key
-      // rows are consecutive too: a request's rows start on a multiple of 8,
-      // and so do its suffix key rows); padding rows get zeros, so attention
-      // reads inert values past a request's last key
+      // V^T (col, krow(m)): 8 consecutive rows of one column per item (their key
+      // rows are consecutive and inside one key tile: a request's rows start
+      // on a multiple of 8, and so do its suffix key rows); padding rows get
+      // zeros, so attention reads inert values past a request's last key
       const int rchunks = rows / 8;
       for (int it = tid; it < BN * rchunks; it += NT) {
         const int c = it % BN, rc = it / BN;
@@ -348,7 +348,7 @@ __device__ __forceinline__ void epi_qkv(float* sC, int ldc, int rows, int m_base
 #pragma unroll
         for (int i = 0; i < 8; ++i) v[i] = e.slot[m0 + i] < 0 ? 0.0f : src[(int64_t)i * ldc];
         const int64_t kr0 = e.krow != nullptr ? e.krow[m0] : m0;
-        store8(reinterpret_cast<T*>(e.vt) + (int64_t)(vbase + c) * e.ldvt + kr0, v);
+        store8(reinterpret_cast<T*>(e.vt) + vt_offset(vbase + c, kr0, e.ldvt, d), v);
       }
     }
   }

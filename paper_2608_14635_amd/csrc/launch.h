@@ -26,7 +26,7 @@ struct EpiParams {
   void* q_out;            // [rows][nq*d]
   void* arena_k;          // this layer's K plane: [slots][nkv][d]
   void* arena_v;          // this layer's V plane
-  void* vt;               // V^T [nkv*d][ldvt] (bf16 path) or null; row m at column krow(m)
+  void* vt;               // V^T (bf16 path, vt_offset layout) or null; row m at key krow(m)
   int64_t ldvt;
   void* kc;               // K copy [nkv][ldvt][d] (bf16 path) or null; row m at row krow(m)
   const int32_t* krow;    // per row: its key row in kc/vt (null = the row itself)
@@ -113,7 +113,7 @@ struct AttnParams {
   const void* q;          // [rows][nq*d]
   const void* arena_k;    // this layer's K plane
   const void* arena_v;    // this layer's V plane (fp32 path)
-  const void* vt;         // V^T [nkv*d][ldvt] (bf16 path)
+  const void* vt;         // V^T (bf16 path, vt_offset layout)
   int64_t ldvt;
   const void* kc;         // K copy [nkv][ldvt][d] (bf16 path)
   const int64_t* kslot;   // per key row: arena slot (fp32 path reads the arena)
@@ -132,6 +132,18 @@ inline int attn_qblock(int dtype, int group) {
 }
 constexpr int ATTN_QBLOCK_MIN = 32;
 constexpr int ROW_ALIGN = 64;  // each request's rows start on this boundary of the wave
+
+// The V^T copy of the bf16 attention, per kv head: key tiles of VT_KEYS keys,
+// each tile stored as [d][VT_KEYS] contiguously (16 KB at d = 128), so that a
+// tile is one contiguous read and the QKV epilogue's writes of one tile stay
+// in one DRAM region.  Offset (elements) of column col = kvh * d + e, key row
+// `key`, for ldvt key rows per head (a multiple of VT_KEYS).
+constexpr int VT_KEYS = 64;
+__host__ __device__ __forceinline__ int64_t vt_offset(int col, int64_t key, int64_t ldvt, int d) {
+  const int kvh = col / d, e = col % d;
+  return (int64_t)kvh * d * ldvt + (key / VT_KEYS) * (int64_t)d * VT_KEYS + (int64_t)e * VT_KEYS +
+         key % VT_KEYS;
+}
 void launch_attention_bf16(const AttnParams& p, hipStream_t s);
 // Prefix keys of a rebuild from a retained prefix: segment (key row, count
 // <= 64) copies the arena K/V of those key rows' slots into the K copy and
