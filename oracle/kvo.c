@@ -42,6 +42,7 @@
 #include "kvo.h"
 
 #include <math.h>
+#include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
 #ifdef _OPENMP
@@ -379,12 +380,21 @@ int kvo_rebuild_from(const kvo_model* m, const void* embed, const kvo_layer* lay
   return 0;
 }
 
+/* Progress lines on stderr, one per layer of every request of at least 256
+ * tokens, when the environment sets KVO_PROGRESS=1 (long test runs report
+ * that they are alive); nothing else depends on it. */
+static int progress_on(void) {
+  const char* e = getenv("KVO_PROGRESS");
+  return e != NULL && e[0] == '1';
+}
+
 int kvo_rebuild(const kvo_model* m, const void* embed, const kvo_layer* layers,
                 const int32_t* tokens, const int32_t* lens, int32_t num_requests,
                 const int32_t* block_tables, int32_t max_blocks, kvo_arena* arena,
                 double* final_hidden) {
   int64_t off = 0;
   int32_t r;
+  const int progress = progress_on();
   if (check_args(m, tokens, lens, num_requests, block_tables, max_blocks, arena)) return -1;
   for (r = 0; r < num_requests; ++r) {
     const int64_t n = lens[r], H = m->hidden;
@@ -398,6 +408,11 @@ int kvo_rebuild(const kvo_model* m, const void* embed, const kvo_layer* layers,
     for (l = 0; l < m->num_layers; ++l) {
       const int kv_only = (l == m->num_layers - 1) && final_hidden == NULL;
       layer_step(m, &layers[l], l, x, 0, n, table, arena, kv_only, scratch);
+      if (progress && n >= 256) {
+        fprintf(stderr, "[oracle] request %d (%lld tokens): layer %d of %d\n", (int)r, (long long)n, l + 1,
+                m->num_layers);
+        fflush(stderr);
+      }
     }
     if (final_hidden) memcpy(final_hidden + off * H, x, sizeof(double) * (size_t)(n * H));
     free(scratch);
