@@ -54,6 +54,9 @@ if LONG:
     CASES["llama8b_300"] = (W.LLAMA8B, [1, 17, 300])
     CASES["qwen14b_300"] = (W.QWEN14B, [1, 17, 300])
     CASES["qwen32b_300"] = (W.QWEN32B, [1, 17, 300])
+    # the 8B shape with a 1000-token request too: about 12 minutes end to end and
+    # 2 x 9 minutes layer by layer (KVR_DEPTH_LAYERS=0:16, 16:31)
+    CASES["llama8b_1000"] = (W.LLAMA8B, [1, 17, 300, 1000])
 
 
 def say(msg):
@@ -110,7 +113,7 @@ def test_end_to_end_all_layers(oracle_lib, name):
     say(f"  bit-identical share, GPU vs P-rounded oracle: {exact_frac(g, o_p, wl)}")
     say(f"  bit-identical share, GPU vs definition:       {exact_frac(g, o, wl)}")
     envelope = drift
-    if name.startswith("llama8b"):
+    if name in ("llama8b", "llama8b_300"):
         # the oracle against itself with the last bit of one layer-0 value
         # weight flipped: the model's own sensitivity to one rounding-sized change
         w1 = {"embed": host_w["embed"], "layers": [dict(lw) for lw in host_w["layers"]]}
@@ -136,8 +139,8 @@ def test_every_layer_from_common_input(oracle_lib, name):
     # KVR_DEPTH_LAYERS="a:b" checks the pairs l = a..b-1 only (the oracle still
     # forms every earlier layer's input), so a long case can be split over runs
     rng = os.environ.get("KVR_DEPTH_LAYERS", "")
-    if name == "qwen32b_300" and not rng:
-        pytest.skip("the 32B shape's layer-by-layer oracle at 300 tokens takes about 25 minutes; "
+    if name in ("qwen32b_300", "llama8b_1000") and not rng:
+        pytest.skip("this case's layer-by-layer oracle takes about 20-25 minutes; "
                     "run it in parts with KVR_DEPTH_LAYERS")
     shape, lens = CASES[name]
     wl = W.small_workload(shape, lens, block_size=16, seed=421, other_live_frac=0.3)
