@@ -3,22 +3,23 @@
 // bf16 path (head_dim 128): a workgroup is 8 wave64s = HW q heads of one GQA
 // group x QW blocks of 32 queries of one request (HW * QW = 8), so every K/V
 // tile staged in LDS feeds 8 waves.  Key tiles of 64 keys stream into a
-// 3-stage LDS ring with buffer_load_dwordx4 ... lds (two tiles in flight): K rows
-// from a contiguous per-head copy of the stored K, V from the V^T copy (one
-// contiguous 16 KB block per key tile), both written by the QKV epilogue with
-// the values sent to the arena.  Scores are
-// computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: a lane owns
-// one query column and 32 of the tile's keys in registers, so the online
-// softmax statistics are per-lane scalars completed by one cross-half
-// exchange, and P^T feeds O^T = V^T P^T straight from registers as the B
-// operand.  K rows are placed in LDS with bits 2 and 3 of their index swapped,
-// which makes the 8 keys of each P^T operand slot group contiguous in V^T, so
-// every V^T operand is one 16-byte LDS read.  exp2 with the scale folded in;
-// P rounded to bf16 for the MFMA, and the softmax denominator summed from
-// the same rounded values (bf16 dot2 with fp32 accumulation); fp32 accumulation; masking only on tiles
-// that cross a wave's diagonal; the exponents are taken against an integer
-// anchor (log2 units), raised and O rescaled by a power of two only when
-// some lane's max rose by a factor above 2^8 since the last rescale.  q-blocks are
+// 3-stage LDS ring with buffer_load_dwordx4 ... lds (two tiles in flight): K
+// rows from a contiguous per-head copy of the stored K, V from the V^T copy
+// (one contiguous 16 KB block per key tile), both written by the QKV epilogue
+// with the values sent to the arena.  Scores are computed transposed,
+// S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: a lane owns one query column
+// and 32 of the tile's keys in registers, so the online softmax statistics are
+// per-lane scalars completed by one exchange with the lane holding the
+// column's other 32 keys (v_permlane32_swap), and P^T feeds O^T = V^T P^T
+// straight from registers as the B operand.  K rows are placed in LDS with
+// bits 2 and 3 of their index swapped, which makes the 8 keys of each P^T
+// operand slot group contiguous in V^T, so every V^T operand is one 16-byte
+// LDS read.  exp2 with the scale folded in; P rounded to bf16 for the MFMA,
+// and the softmax denominator summed from the same rounded values (bf16 dot2
+// with fp32 accumulation); fp32 accumulation; masking only on tiles that
+// cross a wave's diagonal; the exponents are taken against an integer anchor
+// (log2 units), raised and O rescaled by a power of two only when some lane's
+// max rose by a factor above 2^8 since the last rescale.  q-blocks are
 // scheduled longest-first.  Deterministic: fixed key order, no atomics.
 //
 // fp32 path: a plain online-softmax kernel (one wave per query, lanes across
