@@ -747,7 +747,7 @@ int n_tiles_of(const GemmParams& p) {
   return p.bmap == BMAP_GATEUP ? p.epi.ffn / (BN / 2) : (p.n_end - p.n_begin) / BN;
 }
 
-int group_m_for(int tiles_n) { return tiles_n <= 16 ? 4 : 8; }
+int group_m_for(int tiles_n) { return tiles_n <= 24 ? 4 : 8; }
 
 }  // namespace
 
