@@ -11,7 +11,8 @@ What pins what:
   * textbook PyTorch fp64 forward (library rms_norm / linear / causal GQA
     scaled_dot_product_attention / silu / rotate-half RoPE): whole forward
   * closed forms: Wq = 0 gives uniform causal attention (mean of V rows);
-    position 0 leaves K unrotated
+    position 0 leaves K unrotated; a two-layer worked example whose every
+    K, V and final residual value is derived by hand (golden/worked_example.txt)
   * invariants: prefill == token-by-token decode through the arena; rotary
     pair norms and the rotation angle; relative-position dot products;
     GQA == MHA with duplicated KV heads; causality; batch independence;
@@ -26,8 +27,10 @@ What pins what:
 """
 from __future__ import annotations
 
+import ast
 import dataclasses
 import math
+import operator
 import os
 import sys
 
@@ -204,6 +207,108 @@ def pin_uniform_attention_closed_form(o):
         expect = np.concatenate([mean[:, h // g] for h in range(nq)], axis=1)
         assert np.max(np.abs(u - expect)) <= 1e-12 * max(1.0, np.max(np.abs(expect))), \
             "uniform-attention closed form violated"
+
+
+_EXPR_FUNCS = {"cos": math.cos, "sin": math.sin, "exp": math.exp, "sqrt": math.sqrt}
+_EXPR_OPS = {ast.Add: operator.add, ast.Sub: operator.sub, ast.Mult: operator.mul,
+             ast.Div: operator.truediv, ast.Pow: operator.pow}
+
+
+def _eval_expr(text: str, env: dict) -> float:
+    """Value of a fixture expression: numbers, names bound by earlier `let`
+    lines, + - * / **, unary minus and cos/sin/exp/sqrt of one argument."""
+    def ev(n):
+        if isinstance(n, ast.Constant) and isinstance(n.value, (int, float)):
+            return float(n.value)
+        if isinstance(n, ast.Name):
+            return env[n.id]
+        if isinstance(n, ast.UnaryOp) and isinstance(n.op, ast.USub):
+            return -ev(n.operand)
+        if isinstance(n, ast.BinOp) and type(n.op) in _EXPR_OPS:
+            return _EXPR_OPS[type(n.op)](ev(n.left), ev(n.right))
+        if (isinstance(n, ast.Call) and isinstance(n.func, ast.Name)
+                and n.func.id in _EXPR_FUNCS and len(n.args) == 1 and not n.keywords):
+            return _EXPR_FUNCS[n.func.id](ev(n.args[0]))
+        raise ValueError(f"unsupported expression: {text}")
+    return ev(ast.parse(text.strip(), mode="eval").body)
+
+
+def _worked_example(path: str):
+    """Model, weights, requests and hand-derived expectations of the worked
+    example fixture (its header states the format)."""
+    kw, arena, reqs, embed, weights, env, expect = {}, {}, [], {}, {}, {}, []
+    for raw in open(path):
+        line = raw.split("#", 1)[0].strip()
+        if not line:
+            continue
+        word, _, rest = line.partition(" ")
+        if word in ("shape", "arena"):
+            for item in rest.split():
+                k, v = item.split("=")
+                (kw if word == "shape" else arena)[k] = float(v)
+        elif word == "request":
+            f = dict(item.split("=") for item in rest.split())
+            reqs.append(([int(t) for t in f["tokens"].split(",")],
+                         [int(b) for b in f["blocks"].split(",")]))
+        elif word == "let":
+            name, _, expr = rest.partition("=")
+            env[name.strip()] = _eval_expr(expr, env)
+        else:
+            head, _, values = line.partition(":")
+            head = head.split()
+            if word == "embed":
+                embed[int(head[1])] = [float(x) for x in values.split()]
+            elif word == "weight":
+                rows = [[float(x) for x in r.split()] for r in values.split("|")]
+                weights[(int(head[1]), head[2])] = np.array(rows if len(rows) > 1 else rows[0])
+            elif word in ("K", "V", "hidden"):
+                key = tuple(int(x) for x in head[1:])
+                expect.append((word, key, [_eval_expr(e, env) for e in values.split(",")]))
+            else:
+                raise ValueError(f"unknown fixture line: {line}")
+    shape = W.ModelShape(int(kw["layers"]), int(kw["hidden"]), int(kw["q_heads"]),
+                         int(kw["kv_heads"]), int(kw["head_dim"]), int(kw["ffn"]),
+                         int(kw["vocab"]), kw["eps"], kw["theta"], F64)
+    w = {"embed": np.array([embed[t] for t in range(shape.vocab)], np.float64),
+         "layers": [{k: np.ascontiguousarray(weights[(l, k)], np.float64) for k in W.LAYER_KEYS}
+                    for l in range(shape.num_layers)]}
+    B, NB = int(arena["block_size"]), int(arena["num_blocks"])
+    max_blocks = max(len(b) for _, b in reqs)
+    tables = np.full((len(reqs), max_blocks), -1, np.int32)
+    for r, (_, b) in enumerate(reqs):
+        tables[r, :len(b)] = b
+    wl = W.Workload("worked_example", shape, np.array([len(t) for t, _ in reqs], np.int32),
+                    np.array([t for toks, _ in reqs for t in toks], np.int32), B, NB, max_blocks,
+                    tables, np.zeros(0, np.int64), 0)
+    return shape, w, wl, expect
+
+
+def pin_worked_example_by_hand(o):
+    """Every K and V the rebuild writes, and the residual after the last layer,
+    of a two-layer model equal to values derived by hand in closed form (fp64
+    mode); every other arena element keeps its fill value."""
+    shape, w, wl, expect = _worked_example(os.path.join(os.path.dirname(__file__), "golden",
+                                                       "worked_example.txt"))
+    fill = -7.0
+    arena = np.full(wl.arena_elems(), fill, np.float64)
+    a, fh = run(o, shape, w, wl, arena=arena, final_hidden=True)
+    v = view(wl, shape, a)
+    off = wl.request_offsets()
+    seen = np.zeros(v.shape[:4], bool)
+    for kind, key, want in expect:
+        if kind == "hidden":
+            r, p = key
+            got = fh[off[r] + p]
+        else:
+            l, r, p = key
+            blk, slot = wl.block_tables[r, p // wl.block_size], p % wl.block_size
+            got = v[l, 0 if kind == "K" else 1, blk, slot].reshape(-1)
+            seen[l, 0 if kind == "K" else 1, blk, slot] = True
+        want = np.array(want)
+        assert np.all(np.abs(got - want) <= 1e-12 * np.maximum(1.0, np.abs(want))), \
+            f"worked example {kind} {key}: oracle {got} vs hand-derived {want}"
+    assert np.array_equal(seen, written_mask(wl, shape)), "worked example does not cover every written slot"
+    assert np.all(v[~seen] == fill), "worked example: an unlisted arena element changed"
 
 
 def pin_position0_unrotated(o):
