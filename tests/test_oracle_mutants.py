@@ -89,6 +89,34 @@ MUTANTS = [
      "        den += exp2(z[j] * M_LOG2E - c);\n        z[j] = rnd(to_work(exp2(z[j] * M_LOG2E - c), dt), dt);", 0),
     ("round_p_anchored_at_the_exact_max", "const double c = ceil(zmax * M_LOG2E);",
      "const double c = zmax * M_LOG2E;", 0),
+    # causal mask, norm, rotation, gather and projection mix-ups
+    ("causal_mask_one_key_ahead", "kvh = h / g, p = p0 + r;",
+     "kvh = h / g, p = (r + 1 < cnt) ? p0 + r + 1 : p0 + r;", 0),
+    ("causal_mask_without_the_diagonal", "kvh = h / g, p = p0 + r;", "kvh = h / g, p = p0 + r - 1;", 0),
+    ("norm_eps_outside_the_root", "inv = 1.0 / sqrt(ss / (double)H + eps);",
+     "inv = 1.0 / (sqrt(ss / (double)H) + eps);", 0),
+    ("ffn_norm_with_attention_gain", "rmsnorm(x, lw->ffn_norm, dt, H, m->rms_eps, cnt, a);",
+     "rmsnorm(x, lw->attn_norm, dt, H, m->rms_eps, cnt, a);", 0),
+    ("q_not_rotated", "rope_row(q + r * nq * d, (int)nq, (int)d, p, m->rope_theta, dt);", ";", 0),
+    ("v_rotated", "rope_row(k + r * nkv * d, (int)nkv, (int)d, p, m->rope_theta, dt);",
+     "rope_row(k + r * nkv * d, (int)nkv, (int)d, p, m->rope_theta, dt);\n"
+     "    rope_row(v + r * nkv * d, (int)nkv, (int)d, p, m->rope_theta, dt);", 0),
+    ("embedding_row_off_by_one", "load(embed, m->dtype, (int64_t)tok[r] * H + j)",
+     "load(embed, m->dtype, (((int64_t)tok[r] + 1) % m->vocab) * H + j)", 0),
+    ("wo_transposed", "project(lw->wo, dt, H, nq * d, u, cnt, a);",
+     "if (H == nq * d) {\n"
+     "    for (idx = 0; idx < cnt * H; ++idx) {\n"
+     "      const int64_t rr = idx / H, ii = idx % H;\n"
+     "      double s = 0.0;\n"
+     "      int64_t kk;\n"
+     "      for (kk = 0; kk < H; ++kk) s += load(lw->wo, dt, kk * H + ii) * u[rr * H + kk];\n"
+     "      a[idx] = to_work(s, dt);\n"
+     "    }\n"
+     "  } else project(lw->wo, dt, H, nq * d, u, cnt, a);", 0),
+    ("down_reads_up_not_swiglu", "project(lw->w_down, dt, H, F, gate, cnt, a);",
+     "project(lw->w_down, dt, H, F, up, cnt, a);", 0),
+    ("k_written_to_layer_zero", "store(ar->base, dt, arena_off(m, ar, l, 0, slot) + e",
+     "store(ar->base, dt, arena_off(m, ar, 0, 0, slot) + e", 0),
 ]
 
 
