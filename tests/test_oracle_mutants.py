@@ -117,6 +117,10 @@ MUTANTS = [
      "project(lw->w_down, dt, H, F, up, cnt, a);", 0),
     ("k_written_to_layer_zero", "store(ar->base, dt, arena_off(m, ar, l, 0, slot) + e",
      "store(ar->base, dt, arena_off(m, ar, 0, 0, slot) + e", 0),
+    # RoPE precision: the angle in fp64, cos and sin rounded once to the working precision
+    ("rope_cos_sin_unrounded", "if (dt != KVO_F64) { c = (double)(float)c; s = (double)(float)s; }", ";", 0),
+    ("rope_angle_in_fp32", "double phi = (double)pos * inv_freq;",
+     "double phi = (double)((float)pos * (float)inv_freq);", 0),
 ]
 
 
