@@ -121,6 +121,14 @@ MUTANTS = [
     ("rope_cos_sin_unrounded", "if (dt != KVO_F64) { c = (double)(float)c; s = (double)(float)s; }", ";", 0),
     ("rope_angle_in_fp32", "double phi = (double)pos * inv_freq;",
      "double phi = (double)((float)pos * (float)inv_freq);", 0),
+    # the layer-0 K/V helper that samples expected rows at full size
+    ("layer0_helper_without_eps", "inv = 1.0 / sqrt(ss / (double)H + m->rms_eps);",
+     "inv = 1.0 / sqrt(ss / (double)H);", 0),
+    ("layer0_helper_gain_dropped", "a[j] = rnd(load(layer0->attn_norm, dt, j) * x[j] * inv, dt);",
+     "a[j] = rnd(x[j] * inv, dt);", 0),
+    ("layer0_helper_position_zero",
+     "rope_row(k, m->num_kv_heads, m->head_dim, positions[i], m->rope_theta, dt);",
+     "rope_row(k, m->num_kv_heads, m->head_dim, 0, m->rope_theta, dt);", 0),
 ]
 
 
