@@ -51,6 +51,8 @@ def compare(wl: W.Workload, gpu_bits: np.ndarray, ora_bits: np.ndarray, before_b
             for h in range(s.num_kv_heads):
                 den = np.max(np.abs(ov[:, h]))
                 err = np.max(np.abs(gv[:, h] - ov[:, h])) / (den if den > 0 else 1.0)
+                if not np.isfinite(err):
+                    err = np.inf  # a NaN would otherwise vanish in max() below
                 worst[l, kv] = max(worst[l, kv], err)
     report["worst"] = float(worst.max()) if worst.size else 0.0
     return worst, report
