@@ -109,7 +109,8 @@ def normwise(g, o):
     g = np.asarray(g, np.float64)
     o = np.asarray(o, np.float64)
     den = np.max(np.abs(o))
-    return float(np.max(np.abs(g - o)) / den) if den > 0 else float(np.max(np.abs(g - o)))
+    err = float(np.max(np.abs(g - o)) / den) if den > 0 else float(np.max(np.abs(g - o)))
+    return err if np.isfinite(err) else np.inf  # NaN would vanish in a max() fold
 
 
 # ----------------------------------------------------------------------

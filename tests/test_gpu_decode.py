@@ -119,7 +119,8 @@ def slot_rows(wl, arena_bits, positions):
 def rel(g, o):
     g, o = np.asarray(g, np.float64), np.asarray(o, np.float64)
     den = np.max(np.abs(o))
-    return float(np.max(np.abs(g - o)) / (den if den > 0 else 1.0))
+    err = float(np.max(np.abs(g - o)) / (den if den > 0 else 1.0))
+    return err if np.isfinite(err) else np.inf  # NaN would vanish in a max() fold
 
 
 def assert_valid_argmax(gpu_tok, ora_logits, tol):

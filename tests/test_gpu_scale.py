@@ -81,7 +81,8 @@ class NormErr:
         self.total += g_bits.size
 
     def err(self):
-        return float(np.max(self.num / np.where(self.den > 0, self.den, 1.0)))
+        err = float(np.max(self.num / np.where(self.den > 0, self.den, 1.0)))
+        return err if np.isfinite(err) else np.inf  # NaN would vanish in a max() fold
 
     def exact(self):
         return self.same / max(1, self.total)
